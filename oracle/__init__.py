@@ -1,0 +1,137 @@
+"""Plain CPU oracle for paged causal attention -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its Python binding) never imports, links or calls it, and the oracle imports
+nothing from the product.
+
+The arithmetic lives in ``vd_oracle.c`` (IEEE double, plain loops, ascending
+sums), which follows the problem statement of the paper's Appendix A.1 and the
+causal contract of Section 5.3: row ``i`` of a request with query length ``s``
+and key length ``n`` is logical position ``p = n - s + i`` and attends to the
+logical keys ``0..p`` gathered through the request's page table.
+
+Pool layout read by the oracle: ``[num_pages, num_kv_heads, page_size,
+head_dim]`` bf16 bit patterns (uint16).  This is the oracle's own plain layout;
+the GPU library keeps its pool in a layout of its own.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "vd_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+ERRORS = {
+    -1: "invalid argument",
+    -2: "invalid lengths (need 0 < s <= n, cu_q_lens consistent, pages fit the table)",
+    -3: "page id out of range",
+    -4: "out of memory / thread start failure",
+}
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc into ``oracle/liboracle.so``."""
+    if not force and os.path.exists(_LIB) and os.path.getmtime(_LIB) >= os.path.getmtime(_SRC):
+        return _LIB
+    tmp = _LIB + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-std=c11", "-fPIC",
+           "-shared", "-pthread", _SRC, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def bind(path: str):
+    """Loads an oracle shared library (the built one, or a test's mutant)."""
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    lib.vdo_paged_attention.restype = ctypes.c_int
+    lib.vdo_paged_attention.argtypes = [
+        ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_int, ctypes.c_double, P, P, P, P, ctypes.c_int, P, P,
+        ctypes.c_int64, P, P, ctypes.c_int]
+    lib.vdo_default_threads.restype = ctypes.c_int
+    return lib
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            build(force=False)
+            _lib = bind(_LIB)
+    return _lib
+
+
+def default_threads() -> int:
+    return int(_load().vdo_default_threads())
+
+
+def _c(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_pool_bits,
+                    *, num_q_heads, num_kv_heads, head_dim, page_size, scale=None,
+                    rows=None, threads=0, lib=None) -> np.ndarray:
+    """Exact (fp64) paged causal attention.
+
+    q_bits:        uint16 [T, Hq, D] bf16 bit patterns, rows packed by request.
+    cu_q_lens:     int32 [B+1] query-row offsets (cu[0] = 0, cu[B] = T).
+    context_lens:  int32 [B] key lengths n_r (count this call's own tokens).
+    page_table:    int32 [B, stride]; the first ceil(n_r / P) entries are used.
+    k/v_pool_bits: uint16 [num_pages, Hkv, P, D] bf16 bit patterns.
+    scale:         softmax scale (default 1/sqrt(D)).
+    rows:          optional iterable of token indices (or bool mask [T]); only
+                   those rows are computed, the rest of the result is NaN.
+    threads:       host threads (0 = all online cores).
+    lib:           an alternative library from ``bind`` (tests of the pins).
+
+    Returns float64 [T, Hq, D].
+    """
+    lib = _load() if lib is None else lib
+    q_bits, qp = _c(q_bits, np.uint16)
+    T = q_bits.shape[0]
+    assert q_bits.shape == (T, num_q_heads, head_dim), q_bits.shape
+    cu, cup = _c(cu_q_lens, np.int32)
+    ctx, ctxp = _c(context_lens, np.int32)
+    pt, ptp = _c(page_table, np.int32)
+    B = ctx.shape[0]
+    assert cu.shape == (B + 1,)
+    pt = pt.reshape(B, -1) if B else pt.reshape(0, 0)
+    stride = pt.shape[1] if B else 0
+    kp, kpp = _c(k_pool_bits, np.uint16)
+    vp, vpp = _c(v_pool_bits, np.uint16)
+    assert kp.shape == vp.shape and kp.ndim == 4
+    assert kp.shape[1:] == (num_kv_heads, page_size, head_dim), kp.shape
+    if scale is None:
+        scale = 1.0 / np.sqrt(head_dim)
+    sel = None
+    selp = None
+    if rows is not None:
+        rows_arr = np.asarray(rows)
+        if rows_arr.dtype == bool:
+            sel = rows_arr.astype(np.uint8)
+        else:
+            sel = np.zeros(T, np.uint8)
+            sel[rows_arr.astype(np.int64)] = 1
+        sel, selp = _c(sel, np.uint8)
+    out = np.full((T, num_q_heads, head_dim), np.nan, np.float64)
+    rc = lib.vdo_paged_attention(
+        B, T, num_q_heads, num_kv_heads, head_dim, page_size, float(scale), qp, cup, ctxp,
+        ptp, stride, kpp, vpp, kp.shape[0], selp, out.ctypes.data_as(ctypes.c_void_p),
+        int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the call: %s (%d)" % (ERRORS.get(rc, "?"), rc))
+    return out
+

@@ -1,0 +1,223 @@
+/*
+ * vd_oracle.c -- plain, slow CPU oracle for paged causal attention.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header, table or helper with the GPU path: it reads bf16 bit patterns and
+ * page tables in its own plain layout and computes in IEEE double.
+ *
+ * What it computes (the problem statement of Appendix A.1 of the paper,
+ * "Properties and Logical Inputs", and the causal contract of Section 5.3):
+ *
+ *   An invocation holds num_seqs requests.  Request r has query length
+ *   s_r = cu_q_lens[r+1] - cu_q_lens[r] and key length n_r = context_lens[r],
+ *   with 0 < s_r <= n_r.  Its query row i (0 <= i < s_r) stands for logical
+ *   position p = n_r - s_r + i.
+ *
+ *   Logical keys and values come from the physical pool through the request's
+ *   page table pi_r:  K[j,:] = Kphys[pi_r(floor(j/P)), kv_head, j mod P, :]
+ *   (the pool here is laid out [page][kv_head][slot][d]).
+ *
+ *   Query head h reads KV head floor(h / (Hq/Hkv)) (contiguous GQA groups;
+ *   the paper does not fix the grouping, this is the usual convention).
+ *
+ *   For each selected row and head:
+ *       score_j = scale * sum_d q[d] * K[j,d]           for j = 0..p
+ *       w_j     = exp(score_j - max_j score) / sum_j exp(score_j - max_j score)
+ *       out[d]  = sum_j w_j * V[j,d]
+ *   which is exactly softmax attention restricted to the causal prefix
+ *   j <= p (the mask of Appendix A.2 reduces to j <= p because p < n).
+ *
+ * Every sum runs in ascending index order in double precision.  No blocking,
+ * no online softmax, no splitting: the definition written out.
+ *
+ * Error behaviour: returns 0 on success, a negative code on invalid input
+ * (nothing is written to `out` for a rejected call).
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+#define VDO_OK 0
+#define VDO_ERR_ARG (-1)
+#define VDO_ERR_LENGTHS (-2)
+#define VDO_ERR_PAGE (-3)
+#define VDO_ERR_NOMEM (-4)
+
+/* bf16 is the top half of an IEEE binary32; widening is exact. */
+static double bf16_to_double(uint16_t bits) {
+  uint32_t u = ((uint32_t)bits) << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+typedef struct {
+  int num_seqs;
+  int64_t total_q_tokens;
+  int hq, hkv, d, page_size;
+  double scale;
+  const uint16_t *q;
+  const int32_t *cu_q_lens, *context_lens, *page_table;
+  int pt_stride;
+  const uint16_t *k_pool, *v_pool;
+  int64_t num_pages;
+  const uint8_t *row_select;
+  double *out;
+  /* work queue over (request, q-head) pairs */
+  int64_t next_item;
+  pthread_mutex_t lock;
+} job_t;
+
+/* One (request, query head) pair: every selected row of that request. */
+static int run_item(job_t *J, int r, int h, double *score, double *w) {
+  const int D = J->d, P = J->page_size;
+  const int group = J->hq / J->hkv;
+  const int g = h / group;
+  const int32_t q0 = J->cu_q_lens[r];
+  const int s = J->cu_q_lens[r + 1] - q0;
+  const int n = J->context_lens[r];
+  const int32_t *pt = J->page_table + (int64_t)r * J->pt_stride;
+
+  for (int i = 0; i < s; ++i) {
+    const int64_t t = (int64_t)q0 + i;
+    if (J->row_select && !J->row_select[t]) continue;
+    const int p = n - s + i; /* logical position of this row */
+    const uint16_t *qrow = J->q + (t * J->hq + h) * (int64_t)D;
+
+    /* scores over the causal prefix j = 0..p */
+    for (int j = 0; j <= p; ++j) {
+      const int64_t page = pt[j / P];
+      const uint16_t *krow =
+          J->k_pool + (((page * J->hkv + g) * P) + (j % P)) * (int64_t)D;
+      double acc = 0.0;
+      for (int dd = 0; dd < D; ++dd)
+        acc += bf16_to_double(qrow[dd]) * bf16_to_double(krow[dd]);
+      score[j] = J->scale * acc;
+    }
+    /* softmax */
+    double mx = -INFINITY;
+    for (int j = 0; j <= p; ++j)
+      if (score[j] > mx) mx = score[j];
+    double denom = 0.0;
+    for (int j = 0; j <= p; ++j) {
+      w[j] = exp(score[j] - mx);
+      denom += w[j];
+    }
+    for (int j = 0; j <= p; ++j) w[j] /= denom;
+    /* weighted sum of values */
+    double *orow = J->out + (t * J->hq + h) * (int64_t)D;
+    for (int dd = 0; dd < D; ++dd) orow[dd] = 0.0;
+    for (int j = 0; j <= p; ++j) {
+      const int64_t page = pt[j / P];
+      const uint16_t *vrow =
+          J->v_pool + (((page * J->hkv + g) * P) + (j % P)) * (int64_t)D;
+      for (int dd = 0; dd < D; ++dd) orow[dd] += w[j] * bf16_to_double(vrow[dd]);
+    }
+  }
+  return 0;
+}
+
+static void *worker(void *arg) {
+  job_t *J = (job_t *)arg;
+  int maxn = 1;
+  for (int r = 0; r < J->num_seqs; ++r)
+    if (J->context_lens[r] > maxn) maxn = J->context_lens[r];
+  double *score = (double *)malloc(sizeof(double) * (size_t)maxn);
+  double *w = (double *)malloc(sizeof(double) * (size_t)maxn);
+  if (!score || !w) {
+    free(score);
+    free(w);
+    return (void *)1;
+  }
+  const int64_t items = (int64_t)J->num_seqs * J->hq;
+  for (;;) {
+    pthread_mutex_lock(&J->lock);
+    int64_t it = J->next_item++;
+    pthread_mutex_unlock(&J->lock);
+    if (it >= items) break;
+    run_item(J, (int)(it / J->hq), (int)(it % J->hq), score, w);
+  }
+  free(score);
+  free(w);
+  return NULL;
+}
+
+/* Validates the logical inputs before anything is computed. */
+static int validate(const job_t *J) {
+  if (J->num_seqs < 0 || J->hq <= 0 || J->hkv <= 0 || J->d <= 0 ||
+      J->page_size <= 0 || J->hq % J->hkv != 0 || J->pt_stride < 0)
+    return VDO_ERR_ARG;
+  if (J->cu_q_lens[0] != 0 || J->cu_q_lens[J->num_seqs] != J->total_q_tokens)
+    return VDO_ERR_LENGTHS;
+  for (int r = 0; r < J->num_seqs; ++r) {
+    const int s = J->cu_q_lens[r + 1] - J->cu_q_lens[r];
+    const int n = J->context_lens[r];
+    if (s < 1 || s > n) return VDO_ERR_LENGTHS;
+    const int npages = (n + J->page_size - 1) / J->page_size;
+    if (npages > J->pt_stride) return VDO_ERR_LENGTHS;
+    for (int b = 0; b < npages; ++b) {
+      const int32_t pg = J->page_table[(int64_t)r * J->pt_stride + b];
+      if (pg < 0 || pg >= J->num_pages) return VDO_ERR_PAGE;
+    }
+  }
+  return VDO_OK;
+}
+
+int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
+                        int num_kv_heads, int head_dim, int page_size,
+                        double scale, const uint16_t *q,
+                        const int32_t *cu_q_lens, const int32_t *context_lens,
+                        const int32_t *page_table, int pt_stride,
+                        const uint16_t *k_pool, const uint16_t *v_pool,
+                        int64_t num_pages, const uint8_t *row_select,
+                        double *out, int num_threads) {
+  if (!q || !cu_q_lens || !context_lens || !page_table || !k_pool || !v_pool ||
+      !out)
+    return VDO_ERR_ARG;
+  job_t J;
+  memset(&J, 0, sizeof J);
+  J.num_seqs = num_seqs;
+  J.total_q_tokens = total_q_tokens;
+  J.hq = num_q_heads;
+  J.hkv = num_kv_heads;
+  J.d = head_dim;
+  J.page_size = page_size;
+  J.scale = scale;
+  J.q = q;
+  J.cu_q_lens = cu_q_lens;
+  J.context_lens = context_lens;
+  J.page_table = page_table;
+  J.pt_stride = pt_stride;
+  J.k_pool = k_pool;
+  J.v_pool = v_pool;
+  J.num_pages = num_pages;
+  J.row_select = row_select;
+  J.out = out;
+  int rc = validate(&J);
+  if (rc != VDO_OK) return rc;
+
+  if (num_threads <= 0) num_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);
+  if (num_threads < 1) num_threads = 1;
+  pthread_mutex_init(&J.lock, NULL);
+  pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)num_threads);
+  if (!th) return VDO_ERR_NOMEM;
+  int started = 0;
+  for (int i = 0; i < num_threads; ++i)
+    if (pthread_create(&th[i], NULL, worker, &J) == 0) ++started;
+  int failed = started == 0;
+  for (int i = 0; i < started; ++i) {
+    void *ret = NULL;
+    pthread_join(th[i], &ret);
+    if (ret) failed = 1;
+  }
+  free(th);
+  pthread_mutex_destroy(&J.lock);
+  return failed ? VDO_ERR_NOMEM : VDO_OK;
+}
+
+/* Number of host threads the oracle uses when asked for "all cores". */
+int vdo_default_threads(void) { return (int)sysconf(_SC_NPROCESSORS_ONLN); }
