@@ -1,0 +1,252 @@
+"""Benchmark of the paged-attention hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: the KV-cache write of
+the batch's new tokens (vd_kv_write) followed by attention (the split, chunk
+and merge phases of vd_attn_forward), on synthetic bf16 inputs already
+resident in HBM.  R replicas of the inputs (pools, page tables, queries) are
+cycled so that no step finds its K/V in the 256 MB last-level cache left
+behind by the previous step.
+
+Prints one JSON line: whole-step KV GB/s (algorithmic K+V bytes of the batch
+over the step time), the roofline of the dominant kernel measured with HIP
+events on the launch stream, and the CPU oracle timed on the host as a
+reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, vendor figure
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def workloads():
+    from paper_2609_38981_amd import workloads as W
+    return {
+        "decode8b": (lambda: W.config2(pool_factor=1.5),
+                     "Llama-3-8B paged decode: 64 requests, context U[512,4096], Hq 32 / Hkv 8, "
+                     "head_dim 128, page 16, pool 1.5x need"),
+        "mixed8b": (lambda: W.config3(),
+                    "Llama-3-8B mixed batch: 8 prefill chunks of 512 at offsets U[0,8192] + 120 "
+                    "decodes with context U[256,8192], Hq 32 / Hkv 8, head_dim 128, page 16"),
+        "longdecode8b": (lambda: W.config4(),
+                         "Llama-3-8B long-context decode: 8 requests, context U[32768,131072], "
+                         "Hq 32 / Hkv 8, head_dim 128, page 16"),
+        "verify70b": (lambda: W.config5(),
+                      "Llama-70B prefix-shared verify: 256 requests on a shared 2048-token prefix "
+                      "+ suffix U[64,512], s=4 (even) / s=1 (odd), Hq 64 / Hkv 8, head_dim 128"),
+        "tiny": (lambda: W.config1(), "tiny: 2 requests (n 37 s 1, n 100 s 8), Hq 4 / Hkv 2, D 64"),
+    }
+
+
+def host_threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    cap = os.environ.get("OMP_NUM_THREADS")
+    if cap and cap.isdigit():
+        n = min(n, int(cap))
+    return max(n, 1)
+
+
+def cpu_baseline(call, min_seconds: float = 10.0, max_requests: int = 64):
+    """The oracle on the host on a bounded sample of the same workload: the
+    first requests of the batch (whole requests), repeated until at least
+    ``min_seconds`` of wall time.  Returns KV GB/s of the sample."""
+    import oracle
+    from paper_2609_38981_amd import workloads as W
+
+    sh = call.shape
+    # bound the sample: whole requests until ~4 G multiply-adds of attention work
+    reqs, work = [], 0
+    for r in call.reqs[:max_requests]:
+        cost = r.s * r.n * sh.num_q_heads * sh.head_dim * 2
+        if reqs and work + cost > 4e9:
+            break
+        reqs.append(r)
+        work += cost
+    sub = W.Call(sh, call.prompts, reqs, call.page_table[:len(reqs)], call.num_pages,
+                 call.page_owner)
+    kp, vp = call.std_pool(poison=False)
+    args = (sub.q_bits(), sub.cu_q_lens, sub.context_lens, sub.page_table, kp, vp)
+    kw = dict(num_q_heads=sh.num_q_heads, num_kv_heads=sh.num_kv_heads, head_dim=sh.head_dim,
+              page_size=sh.page_size)
+    threads = host_threads()
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.paged_attention(*args, threads=threads, **kw)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or reps >= 1000:
+            break
+    sec = el / reps
+    return {"value": round(sub.kv_bytes() / sec / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d of %d requests (%d query rows, %.1f MB K+V), %d repetitions, %.2f s "
+                      "per repetition" % (len(reqs), call.num_seqs, sub.total_q_tokens,
+                                          sub.kv_bytes() / 1e6, reps, sec)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="decode8b", choices=sorted(workloads()))
+    ap.add_argument("--replicas", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the kernel is "
+              "shown on one GPU's share; see the sharding notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_38981_amd import staging as S
+
+    torch.cuda.set_device(0)
+    make, desc = workloads()[args.workload]
+    t0 = time.perf_counter()
+    call = make()
+    sh = call.shape
+    log("workload %s: %d requests, %d query rows, %.1f MB K+V (%.1fs to generate)" % (
+        args.workload, call.num_seqs, call.total_q_tokens, call.kv_bytes() / 1e6,
+        time.perf_counter() - t0))
+    attn = S.handle_for(sh)
+
+    # replicas of every device input
+    reps = []
+    for i in range(max(args.replicas, 1)):
+        dc = S.to_device(attn, call, poison=False)
+        ws = attn.new_workspace(call.num_seqs, dc.batch.max_q_len, dc.batch.max_context_len)
+        reps.append((dc, ws, torch.empty_like(dc.batch.q)))
+    # this step's new tokens: positions n - s .. n - 1 of every request
+    P = sh.page_size
+    kn, vn, slots = [], [], []
+    for ri, r in enumerate(call.reqs):
+        pr = call.prompts[r.prompt]
+        for p in r.positions:
+            kn.append(pr.k[p])
+            vn.append(pr.v[p])
+            slots.append(int(call.page_table[ri, p // P]) * P + p % P)
+    k_new = S.bf16_tensor(np.stack(kn), "cuda")
+    v_new = S.bf16_tensor(np.stack(vn), "cuda")
+    slot_t = torch.tensor(slots, dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    log("staged %d replicas" % len(reps))
+
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        dc, ws, out = reps[i % len(reps)]
+        b = dc.batch
+        if ev is not None:
+            ev[0].record(stream)
+        attn.kv_write(k_new, v_new, slot_t, b.k_pool, b.v_pool, b.num_pages, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        attn.forward_splits(b, ws, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        attn.forward_chunks(b, out, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+        attn.forward_merge(b, out, ws, stream=stream)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = elapsed * 1e3 / args.steps
+    phase = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in evs])  # ms
+    ph_ms = phase.mean(axis=0)
+    log("phases (ms): kv_write %.4f splits %.4f chunks %.4f merge %.4f; wall %.4f" % (
+        *ph_ms, ms))
+
+    kv_bytes = call.kv_bytes()
+    T = call.total_q_tokens
+    hq, hkv, D = sh.num_q_heads, sh.num_kv_heads, sh.head_dim
+    npages = int(sum(-(-r.n // P) for r in call.reqs))
+    q_bytes = T * hq * D * 2
+    o_bytes = T * hq * D * 2
+    pt_bytes = npages * 4
+    value = kv_bytes / (ms * 1e-3) / 1e9
+
+    # dominant kernel: the split kernel for decode-class batches, the chunk
+    # kernel when chunk rows dominate
+    split_ms, chunk_ms = ph_ms[1], ph_ms[2]
+    if chunk_ms > split_ms:
+        flops = 0
+        for r in call.reqs:
+            if r.s * sh.group > 32:
+                flops += sum(p + 1 for p in r.positions) * hq * D * 4
+        ach = flops / (chunk_ms * 1e-3) / 1e12
+        roof = {"kernel": "chunk_kernel", "bound": "mfma", "achieved": round(ach, 3),
+                "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFS, 4), "traffic": None,
+                "avg_ms": round(float(chunk_ms), 5)}
+    else:
+        split_rows = [r for r in call.reqs if r.s * sh.group <= 32]
+        alg = sum(r.n for r in split_rows) * hkv * D * 2 * 2 + \
+            sum(r.s for r in split_rows) * hq * D * 2 + \
+            sum(-(-r.n // P) for r in split_rows) * 4
+        ach = alg / (split_ms * 1e-3) / 1e9
+        roof = {"kernel": "split_kernel", "bound": "hbm", "achieved": round(ach, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                "traffic": None, "avg_ms": round(float(split_ms), 5),
+                "algorithmic_bytes": int(alg)}
+
+    res = {
+        "metric": "paged-attn KV GB/s (% HBM peak) at bitwise batch/chunk/page invariance",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": desc, "num_seqs": call.num_seqs, "query_rows": T,
+                   "kv_bytes": kv_bytes, "replicas": len(reps)},
+        "hbm_frac_whole_step": round(value / HBM_PEAK_GBS, 4),
+        "tokens_per_s": round(T / (ms * 1e-3), 1),
+        "phase_ms": {"kv_write": round(float(ph_ms[0]), 5), "splits": round(float(ph_ms[1]), 5),
+                     "chunks": round(float(ph_ms[2]), 5), "merge": round(float(ph_ms[3]), 5)},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle baseline")
+        res["cpu_baseline"] = cpu_baseline(call)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

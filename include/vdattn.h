@@ -1,0 +1,175 @@
+/*
+ * vdattn.h -- batch-invariant paged causal attention for AMD MI355X (gfx950).
+ *
+ * C ABI of libvdattn.so.  Plain pointers and sizes only.
+ *
+ * What the library computes
+ * -------------------------
+ * The paper's problem statement (Appendix A.1, "Properties and Logical
+ * Inputs") and causal contract (Section 5.3): an invocation packs the query
+ * rows of num_seqs requests.  Request r has query length s_r and key length
+ * n_r with 0 < s_r <= n_r; its query row i (0 <= i < s_r) stands for logical
+ * position p = n_r - s_r + i.  Logical keys and values are read through the
+ * request's page table pi_r: K[j] = Kphys[pi_r(floor(j / P)), slot j mod P].
+ * Query head h reads KV head floor(h / (Hq / Hkv)).  The output row is softmax
+ * attention of the query over keys 0..p (causal prefix), computed with the
+ * tiled online-softmax update of Appendix A.2 ("A Simplified Tile IR") in
+ * fp32 with bf16 inputs and a bf16 output.
+ *
+ * Guarantee (the causal contract of Section 5.3 / Appendix A.1): the output
+ * bits of a row depend only on (p, the row's query, K/V at positions 0..p,
+ * the handle).  They do not depend on s_r, n_r, the row index, the other
+ * requests of the call, their order, the page table (physical placement,
+ * stride, sharing of pages between requests), num_pages, the hints, the
+ * workspace contents or the stream.  Keys are processed in tiles of 64
+ * logical positions and in splits of 512 logical positions whose partial
+ * states are merged in ascending split order; both sizes are fixed by the
+ * handle, never by the batch.
+ *
+ * Ownership and threading
+ * -----------------------
+ * Every buffer is caller-owned device memory (except the descriptor and the
+ * hints, which are host values).  The library never allocates or frees
+ * device memory, never synchronises the device, and keeps no mutable global
+ * state.  A handle is immutable after creation and may be used from several
+ * host threads and streams at once; concurrent calls must not share a
+ * workspace.
+ *
+ * Errors
+ * ------
+ * Every entry point returns VD_OK (0) or a negative vd_status.  Arguments the
+ * host can see are checked before anything is launched; on such an error no
+ * output is touched.  Device-side data (lengths, page ids) is not read by the
+ * host; the kernels never access memory outside the buffers described below:
+ * a request whose lengths violate 0 < s <= n, whose page count exceeds the
+ * table stride, whose lengths exceed the hints, or whose rows fall outside
+ * total_q_tokens is skipped (its output rows are left unwritten), and a page
+ * id outside [0, num_pages) reads as zeros.
+ */
+#ifndef VDATTN_H
+#define VDATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VD_ABI_VERSION 1
+
+typedef enum {
+  VD_OK = 0,
+  VD_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad descriptor field */
+  VD_ERR_UNSUPPORTED = -2, /* head_dim not in {64, 128}, page_size != 16, dtype != bf16,
+                              Hq not a multiple of Hkv, group size > 32; the paper's
+                              "reject a missing configuration" (Section 1) */
+  VD_ERR_WORKSPACE = -3,   /* workspace missing or smaller than vd_attn_workspace_size */
+  VD_ERR_LAUNCH = -4       /* a kernel launch failed (hipGetLastError) */
+} vd_status;
+
+#define VD_DTYPE_BF16 1
+
+/* Fixed per-model configuration, bound once (Section 4.1, "Fixed kernel
+ * choices": tiles and specialisations are chosen at initialisation and never
+ * from the batch). */
+typedef struct {
+  int32_t abi_version;  /* VD_ABI_VERSION */
+  int32_t num_q_heads;  /* Hq  >= 1 */
+  int32_t num_kv_heads; /* Hkv >= 1, divides Hq, Hq / Hkv <= 32 */
+  int32_t head_dim;     /* D in {64, 128} */
+  int32_t page_size;    /* P, must be 16 */
+  int32_t dtype;        /* VD_DTYPE_BF16: Q, K, V and the output are bf16 */
+  float softmax_scale;  /* <= 0 selects 1 / sqrt(head_dim) */
+} vd_attn_desc;
+
+typedef struct vd_attn vd_attn; /* opaque, immutable after creation */
+
+/* Creates a handle.  *out receives it on success (and NULL on error). */
+int vd_attn_create(const vd_attn_desc* desc, vd_attn** out);
+
+/* Destroys a handle (NULL is accepted). */
+void vd_attn_destroy(vd_attn* h);
+
+/* One call's packed inputs.  Pointers are device memory unless noted. */
+typedef struct {
+  int32_t num_seqs;             /* B >= 0 */
+  int64_t total_q_tokens;       /* T = cu_q_lens[B] >= 0 */
+  const void* q;                /* [T, Hq, D] bf16, rows packed by request, i ascending */
+  const int32_t* cu_q_lens;     /* [B + 1], cu[0] = 0, s_r = cu[r + 1] - cu[r] */
+  const int32_t* context_lens;  /* [B], n_r (counts this call's own query tokens) */
+  const int32_t* page_table;    /* [B * pt_stride]; entries 0 .. ceil(n_r / 16) - 1 of row r used */
+  int32_t pt_stride;            /* >= 1 */
+  const void* k_pool;           /* pools in the library layout (see vd_kv_write), */
+  const void* v_pool;           /*   num_pages pages of Hkv page blocks each */
+  int64_t num_pages;            /* >= 1 */
+  int32_t max_q_len;            /* HOST hint: >= every s_r (launch sizing only) */
+  int32_t max_context_len;      /* HOST hint: >= every n_r (launch sizing only) */
+} vd_attn_batch;
+
+/* Bytes of workspace one call needs for the given host-side sizes. */
+int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
+                           int32_t max_context_len, size_t* bytes);
+
+/* Paged causal attention for every row of the batch (Appendix A.2 update,
+ * Section 5.3 contract).  `out` is device [T, Hq, D] bf16.  The K/V of this
+ * call's own tokens must already be in the pool (vd_kv_write).  The workspace
+ * holds split partial states; its prior contents do not matter.  Launches on
+ * `stream` and returns without waiting. */
+int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/* The three phases vd_attn_forward runs, in this order, for callers that time
+ * or schedule them separately (same arguments, same stream, same workspace;
+ * their composition is bit-identical to vd_attn_forward):
+ *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item per
+ *           (request, KV head, 512-key split); writes partial states;
+ *   chunks: rows of requests with s_r * (Hq / Hkv) > 32 -- one work item per
+ *           (request, KV head, 128 query-head rows); folds the splits in
+ *           registers and writes their output rows;
+ *   merge:  folds the partial states of the split-phase rows in ascending
+ *           split order and writes their output rows. */
+int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* batch, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* batch, void* out,
+                           hipStream_t stream);
+int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* batch, void* out,
+                          const void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of ONE pool (K or V) holding num_pages pages. */
+int vd_pool_bytes(const vd_attn* h, int64_t num_pages, size_t* bytes);
+
+/* KV-cache write (the engine writes new tokens' K/V to private slots before
+ * attention reads them, Section 4.1 "Separate cache reuse from generation").
+ *
+ * k_new, v_new: device [num_tokens, Hkv, D] bf16 rows.
+ * slot_mapping: device [num_tokens] int64, slot = page * 16 + offset; a
+ *               negative slot skips the token; slots outside
+ *               [0, num_pages * 16) are skipped too.
+ * k_pool, v_pool: device pools of vd_pool_bytes(num_pages) bytes each.
+ *
+ * Pool layout (one "page block" per (page, KV head), 16 * D bf16 elements at
+ * element offset (page * Hkv + kv_head) * 16 * D):
+ *   K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
+ *   V block: element (slot, d) at ((slot / 4) * D + d) * 4 + slot % 4
+ * so that the matrix-core operand of each wavefront is one contiguous load.
+ * Two tokens written to the same slot in one call race (either may win). */
+int vd_kv_write(const vd_attn* h, const void* k_new, const void* v_new,
+                const int64_t* slot_mapping, int64_t num_tokens, void* k_pool, void* v_pool,
+                int64_t num_pages, hipStream_t stream);
+
+/* Static description of a status code (never NULL). */
+const char* vd_status_string(int status);
+
+/* Fixed tiling constants of a handle (host query, for reports and tests):
+ * tile_keys = 64, split_keys = 512, page_size = 16. */
+int vd_attn_tiling(const vd_attn* h, int32_t* tile_keys, int32_t* split_keys,
+                   int32_t* page_size);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VDATTN_H */

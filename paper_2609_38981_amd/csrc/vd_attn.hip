@@ -1,0 +1,654 @@
+// vd_attn.hip -- HIP kernels for gfx950 and the C ABI of libvdattn.so.
+//
+// Three attention kernels run the canonical arithmetic of vd_cas.hpp:
+//   split kernel  one wavefront per (request, KV head, 512-key split) for
+//                 requests with at most 32 query-head rows per KV head
+//                 (decode, verify); K/V go straight from HBM to registers in
+//                 the matrix-core operand layout; writes a partial state.
+//   merge kernel  folds those partial states in ascending split order and
+//                 writes the output rows.
+//   chunk kernel  one workgroup per (request, KV head, 128 query-head rows)
+//                 for longer chunks (prefill); K/V tiles are staged in LDS
+//                 and shared by the 4 wavefronts; splits are folded in
+//                 registers with the same fold as the merge kernel.
+// The work decomposition differs between kernels; the operations applied to
+// any one output row, and their order, do not.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <new>
+
+#include "../../include/vdattn.h"
+#include "vd_cas.hpp"
+
+using namespace vd;
+
+namespace {
+
+struct Params {
+  const uint16_t* q;
+  const int32_t* cu;
+  const int32_t* ctx;
+  const int32_t* pt;
+  const uint16_t* kpool;
+  const uint16_t* vpool;
+  uint16_t* out;
+  float* ws_m;
+  float* ws_z;
+  float* ws_u;
+  int64_t T;
+  int64_t num_pages;
+  int num_seqs, pt_stride, max_q, max_ctx, max_splits, qtiles;
+  int hq, hkv, G;
+  float c;  // softmax scale * log2(e), rounded once to fp32 on the host
+};
+
+struct Req {
+  int q0, s, n;
+  bool valid;
+};
+
+// Reads request r's lengths and decides whether it may be processed without
+// touching memory outside the described buffers.
+__device__ __forceinline__ Req load_req(const Params& P, int r) {
+  Req R;
+  const int q0 = P.cu[r], q1 = P.cu[r + 1], n = P.ctx[r];
+  R.q0 = q0;
+  R.s = q1 - q0;
+  R.n = n;
+  const int npages = (n + kPage - 1) / kPage;
+  R.valid = q0 >= 0 && R.s >= 1 && R.s <= n && (int64_t)q1 <= P.T && R.s <= P.max_q &&
+            n <= P.max_ctx && npages <= P.pt_stride;
+  return R;
+}
+
+// Index of the (page, kv_head) page block, or -1 when the logical page lp is
+// past the request's keys or its id is outside the pool.
+__device__ __forceinline__ int64_t page_block(const Params& P, const int32_t* ptrow, int lp,
+                                              int n, int g) {
+  const int npages = (n + kPage - 1) / kPage;
+  if (lp >= npages) return -1;
+  const int32_t page = ptrow[lp];
+  if (page < 0 || (int64_t)page >= P.num_pages) return -1;
+  return (int64_t)page * P.hkv + g;
+}
+
+template <int D>
+__device__ __forceinline__ const uint16_t* block_ptr(const uint16_t* pool, int64_t pb) {
+  return pool + pb * (int64_t)(kPage * D);
+}
+
+__device__ __forceinline__ u16x8 zero8() { return u16x8{0, 0, 0, 0, 0, 0, 0, 0}; }
+
+// Keeps the 4 bf16 values of slots 4 grp .. 4 grp + 3 whose key is < n.
+__device__ __forceinline__ u16x4 mask4(u16x4 v, int key0, int n) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (key0 + i < n) ? v[i] : (uint16_t)0;
+  return v;
+}
+
+template <int D>
+__device__ __forceinline__ void load_q(const Params& P, u16x8 (&qf)[D / 32], int tok, int head,
+                                       bool valid) {
+  const int grp = __lane_id() >> 4;
+  const uint16_t* base = P.q + ((int64_t)tok * P.hq + head) * D + 8 * grp;
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks)
+    qf[ks] = valid ? *reinterpret_cast<const u16x8*>(base + 32 * ks) : zero8();
+}
+
+// ---------------------------------------------------------------------------
+// split kernel
+// ---------------------------------------------------------------------------
+template <int D, int NB>
+__global__ __launch_bounds__(256) void split_kernel(Params P) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = __lane_id();
+  const int col = lane & 15, grp = lane >> 4;
+  const int64_t item = (int64_t)blockIdx.x * 4 + wave;
+  const int MS = P.max_splits;
+  const int64_t rg = item / MS;
+  const int k = (int)(item % MS);
+  if (rg >= (int64_t)P.num_seqs * P.hkv) return;
+  const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
+  const Req R = load_req(P, r);
+  if (!R.valid) return;
+  const int ncols = R.s * P.G;
+  if (ncols > NB * 16) return;  // chunk path (or a hint violation)
+  const int nsplit = (R.n + kSplitKeys - 1) / kSplitKeys;
+  if (k >= nsplit || nsplit > MS) return;
+
+  int pos[NB];
+  u16x8 qf[NB][D / 32];
+  State<D> st[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int c = nb * 16 + col;
+    const bool v = c < ncols;
+    pos[nb] = v ? R.n - R.s + c / P.G : -1;
+    load_q<D>(P, qf[nb], R.q0 + (v ? c / P.G : 0), g * P.G + (v ? c % P.G : 0), v);
+    state_init(st[nb]);
+  }
+
+  const int32_t* ptrow = P.pt + (int64_t)r * P.pt_stride;
+  const int kt_end = min(k * kTilesPerSplit + kTilesPerSplit, (R.n + kTileKeys - 1) / kTileKeys);
+  for (int kt = k * kTilesPerSplit; kt < kt_end; ++kt) {
+    const int j0 = kt * kTileKeys;
+    int64_t pb[kPagesPerTile];
+#pragma unroll
+    for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g);
+    // K operands: page b, chunk ks -> 16 contiguous bytes per lane
+    u16x8 kf[kPagesPerTile][D / 32];
+#pragma unroll
+    for (int b = 0; b < kPagesPerTile; ++b) {
+      const bool ok = pb[b] >= 0 && j0 + 16 * b + col < R.n;
+      const uint16_t* base = block_ptr<D>(P.kpool, pb[b] < 0 ? 0 : pb[b]) + 8 * lane;
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks)
+        kf[b][ks] = ok ? *reinterpret_cast<const u16x8*>(base + 512 * ks) : zero8();
+    }
+    // V operands: d-block m, half hh -> 8 bytes from each of two pages
+    u16x8 vf[D / 16][2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int b = 2 * hh + e;
+        const int key0 = j0 + 16 * b + 4 * grp;
+        const bool ok = pb[b] >= 0 && key0 < R.n;
+        const uint16_t* base =
+            block_ptr<D>(P.vpool, pb[b] < 0 ? 0 : pb[b]) + 4 * (grp * D + col);
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m) {
+          u16x4 v = ok ? *reinterpret_cast<const u16x4*>(base + 64 * m) : u16x4{0, 0, 0, 0};
+          v = mask4(v, key0, R.n);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) vf[m][hh][4 * e + i] = v[i];
+        }
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      if (nb * 16 >= ncols) break;
+      f32x4 acc[kPagesPerTile];
+      tile_scores<D>(kf, qf[nb], acc);
+      tile_update<D>(st[nb], acc, vf, j0, pos[nb], P.c);
+    }
+  }
+
+  // partial state of split k for every column that has a key in it
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int c = nb * 16 + col;
+    if (pos[nb] < 0 || k > pos[nb] / kSplitKeys) continue;
+    const int64_t pidx = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS + k;
+    if (grp == 0) {
+      P.ws_m[pidx] = st[nb].m;
+      P.ws_z[pidx] = st[nb].z;
+    }
+    float* u = P.ws_u + pidx * D + 4 * grp;
+#pragma unroll
+    for (int m = 0; m < D / 16; ++m) *reinterpret_cast<f32x4*>(u + 16 * m) = st[nb].u[m];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// merge kernel: one workgroup per (request, KV head)
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void merge_kernel(Params P) {
+  const int64_t rg = blockIdx.x;
+  if (rg >= (int64_t)P.num_seqs * P.hkv) return;
+  const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
+  const Req R = load_req(P, r);
+  if (!R.valid) return;
+  const int ncols = R.s * P.G;
+  if (ncols > kSplitCols) return;
+  const int nsplit = (R.n + kSplitKeys - 1) / kSplitKeys;
+  const int MS = P.max_splits;
+  if (nsplit > MS) return;
+  for (int e = threadIdx.x; e < ncols * (D / 2); e += blockDim.x) {
+    const int c = e / (D / 2);
+    const int d = 2 * (e % (D / 2));
+    const int pos = R.n - R.s + c / P.G;
+    const int kp = pos / kSplitKeys + 1;
+    const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS;
+    float M = P.ws_m[p0], Z = P.ws_z[p0];
+    float2 W = *reinterpret_cast<const float2*>(P.ws_u + p0 * D + d);
+    for (int k = 1; k < kp; ++k) {
+      const FoldScalars f = fold_scalars(M, Z, P.ws_m[p0 + k], P.ws_z[p0 + k]);
+      const float2 uk = *reinterpret_cast<const float2*>(P.ws_u + (p0 + k) * D + d);
+      W.x = fold_value(W.x, uk.x, f);
+      W.y = fold_value(W.y, uk.y, f);
+      M = f.M;
+      Z = f.Z;
+    }
+    const float rho = final_scale(Z);
+    const int64_t tok = R.q0 + c / P.G;
+    const int head = g * P.G + c % P.G;
+    uint16_t* o = P.out + (tok * P.hq + head) * D + d;
+    const uint32_t packed = (uint32_t)bf16_out(W.x * rho) | ((uint32_t)bf16_out(W.y * rho) << 16);
+    *reinterpret_cast<uint32_t*>(o) = packed;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// chunk kernel: one workgroup (4 wavefronts x 32 columns) per
+// (request, KV head, 128 query-head rows); K/V tiles staged in LDS.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void chunk_kernel(Params P) {
+  constexpr int NB = 2;
+  constexpr int BLK = kPage * D;  // elements of one page block
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kPagesPerTile][BLK];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = __lane_id();
+  const int col = lane & 15, grp = lane >> 4;
+  const int64_t bid = blockIdx.x;
+  const int qt = (int)(bid % P.qtiles);
+  const int64_t rg = bid / P.qtiles;
+  if (rg >= (int64_t)P.num_seqs * P.hkv) return;
+  const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
+  const Req R = load_req(P, r);
+  if (!R.valid) return;
+  const int ncols = R.s * P.G;
+  if (ncols <= kSplitCols) return;  // split path
+  const int c0 = qt * kChunkCols;
+  if (c0 >= ncols) return;
+  const int cend = min(ncols, c0 + kChunkCols);
+  const int pmax = R.n - R.s + (cend - 1) / P.G;  // last position of the block
+
+  int pos[NB];
+  u16x8 qf[NB][D / 32];
+  State<D> st[NB];
+  float M[NB], Z[NB];
+  f32x4 W[NB][D / 16];
+  int wave_pmax = -1;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int c = c0 + wave * 32 + nb * 16 + col;
+    const bool v = c < cend;
+    pos[nb] = v ? R.n - R.s + c / P.G : -1;
+    load_q<D>(P, qf[nb], R.q0 + (v ? c / P.G : 0), g * P.G + (v ? c % P.G : 0), v);
+    const int clast = min(cend, c0 + wave * 32 + nb * 16 + 16) - 1;
+    if (clast >= c0 + wave * 32 + nb * 16) wave_pmax = max(wave_pmax, R.n - R.s + clast / P.G);
+    M[nb] = 0.f;
+    Z[nb] = 0.f;
+#pragma unroll
+    for (int m = 0; m < D / 16; ++m) W[nb][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int32_t* ptrow = P.pt + (int64_t)r * P.pt_stride;
+  const int nsplit = pmax / kSplitKeys + 1;
+  const int ntiles = pmax / kTileKeys + 1;
+  for (int k = 0; k < nsplit; ++k) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) state_init(st[nb]);
+    const int kt_end = min(k * kTilesPerSplit + kTilesPerSplit, ntiles);
+    for (int kt = k * kTilesPerSplit; kt < kt_end; ++kt) {
+      const int j0 = kt * kTileKeys;
+      __syncthreads();  // the previous tile's readers are done
+      // cooperative copy: 8 page blocks (4 K, 4 V) of BLK elements, 16 B per step
+      for (int ch = threadIdx.x; ch < 2 * kPagesPerTile * (BLK / 8); ch += blockDim.x) {
+        const int blk = ch / (BLK / 8);
+        const int off = (ch % (BLK / 8)) * 8;
+        const int b = blk % kPagesPerTile;
+        const bool isv = blk >= kPagesPerTile;
+        const int64_t pb = page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g);
+        const int kbase = j0 + 16 * b;
+        u16x8 v = zero8();
+        if (pb >= 0) {
+          const uint16_t* src = block_ptr<D>(isv ? P.vpool : P.kpool, pb) + off;
+          v = *reinterpret_cast<const u16x8*>(src);
+          if (!isv) {
+            const int slot = (off / 8) % 16;  // K block: [D/8][16][8]
+            if (kbase + slot >= R.n) v = zero8();
+          } else {
+            const int sg = off / (4 * D);  // V block: [4][D][4]
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              v[e] = (kbase + 4 * sg + (e % 4) < R.n) ? v[e] : (uint16_t)0;
+          }
+        }
+        *reinterpret_cast<u16x8*>(&lds[blk][off]) = v;
+      }
+      __syncthreads();
+      if (wave_pmax < j0) continue;  // no column of this wave sees the tile
+      u16x8 kf[kPagesPerTile][D / 32];
+#pragma unroll
+      for (int b = 0; b < kPagesPerTile; ++b)
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks)
+          kf[b][ks] = *reinterpret_cast<const u16x8*>(&lds[b][512 * ks + 8 * lane]);
+      u16x8 vf[D / 16][2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+          for (int m = 0; m < D / 16; ++m) {
+            const u16x4 v = *reinterpret_cast<const u16x4*>(
+                &lds[kPagesPerTile + 2 * hh + e][4 * (grp * D + 16 * m + col)]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) vf[m][hh][4 * e + i] = v[i];
+          }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        f32x4 acc[kPagesPerTile];
+        tile_scores<D>(kf, qf[nb], acc);
+        tile_update<D>(st[nb], acc, vf, j0, pos[nb], P.c);
+      }
+    }
+    // fold split k into the running merge for columns that have it
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      if (pos[nb] < 0 || k > pos[nb] / kSplitKeys) continue;
+      if (k == 0) {
+        M[nb] = st[nb].m;
+        Z[nb] = st[nb].z;
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m) W[nb][m] = st[nb].u[m];
+      } else {
+        const FoldScalars f = fold_scalars(M[nb], Z[nb], st[nb].m, st[nb].z);
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) W[nb][m][i] = fold_value(W[nb][m][i], st[nb].u[m][i], f);
+        M[nb] = f.M;
+        Z[nb] = f.Z;
+      }
+    }
+  }
+
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    if (pos[nb] < 0) continue;
+    const int c = c0 + wave * 32 + nb * 16 + col;
+    const float rho = final_scale(Z[nb]);
+    const int64_t tok = R.q0 + c / P.G;
+    const int head = g * P.G + c % P.G;
+    uint16_t* o = P.out + (tok * P.hq + head) * D + 4 * grp;
+#pragma unroll
+    for (int m = 0; m < D / 16; ++m) {
+      u16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = bf16_out(W[nb][m][i] * rho);
+      *reinterpret_cast<u16x4*>(o + 16 * m) = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// KV write: one thread per (token, KV head, 8 consecutive d)
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void kv_write_kernel(const uint16_t* knew, const uint16_t* vnew,
+                                                       const int64_t* slots, int64_t ntok,
+                                                       uint16_t* kpool, uint16_t* vpool,
+                                                       int64_t num_pages, int hkv) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per_tok = (int64_t)hkv * (D / 8);
+  if (id >= ntok * per_tok) return;
+  const int64_t t = id / per_tok;
+  const int hd = (int)(id % per_tok);
+  const int h = hd / (D / 8);
+  const int dc = hd % (D / 8);
+  const int64_t slot = slots[t];
+  if (slot < 0 || slot >= num_pages * kPage) return;
+  const int64_t page = slot / kPage;
+  const int s = (int)(slot % kPage);
+  const int64_t blk = (page * hkv + h) * (int64_t)(kPage * D);
+  const int64_t src = (t * hkv + h) * D + 8 * dc;
+  const u16x8 kv = *reinterpret_cast<const u16x8*>(knew + src);
+  const u16x8 vv = *reinterpret_cast<const u16x8*>(vnew + src);
+  // K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
+  *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + s) * 8) = kv;
+  // V block: element (slot, d) at ((slot / 4) * D + d) * 4 + slot % 4
+#pragma unroll
+  for (int e = 0; e < 8; ++e) vpool[blk + ((int64_t)(s / 4) * D + 8 * dc + e) * 4 + s % 4] = vv[e];
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+struct vd_attn {
+  int32_t hq, hkv, d, page_size, group;
+  float scale;
+  float c;  // scale * log2(e) in fp32
+};
+
+namespace {
+
+int split_nb(const vd_attn* h, int32_t max_q_len) {
+  return (int64_t)max_q_len * h->group <= 16 ? 1 : 2;
+}
+
+size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct WsLayout {
+  size_t m_off, z_off, u_off, total;
+};
+
+WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_context_len) {
+  const int64_t ms = ((int64_t)max_context_len + kSplitKeys - 1) / kSplitKeys;
+  const int64_t n = (int64_t)num_seqs * h->hkv * kSplitCols * (ms < 1 ? 1 : ms);
+  WsLayout L;
+  L.m_off = 0;
+  L.z_off = round_up(n * sizeof(float));
+  L.u_off = L.z_off + round_up(n * sizeof(float));
+  L.total = L.u_off + round_up((size_t)n * h->d * sizeof(float));
+  return L;
+}
+
+int check_batch(const vd_attn* h, const vd_attn_batch* b) {
+  if (!h || !b) return VD_ERR_INVALID_ARG;
+  if (b->num_seqs < 0 || b->total_q_tokens < 0) return VD_ERR_INVALID_ARG;
+  if (b->num_seqs == 0 || b->total_q_tokens == 0) return VD_OK;
+  if (!b->q || !b->cu_q_lens || !b->context_lens || !b->page_table || !b->k_pool || !b->v_pool)
+    return VD_ERR_INVALID_ARG;
+  if (b->pt_stride < 1 || b->num_pages < 1 || b->max_q_len < 1 || b->max_context_len < 1)
+    return VD_ERR_INVALID_ARG;
+  if (b->max_q_len > b->max_context_len) return VD_ERR_INVALID_ARG;
+  return VD_OK;
+}
+
+Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const void* ws) {
+  Params P;
+  P.q = static_cast<const uint16_t*>(b->q);
+  P.cu = b->cu_q_lens;
+  P.ctx = b->context_lens;
+  P.pt = b->page_table;
+  P.kpool = static_cast<const uint16_t*>(b->k_pool);
+  P.vpool = static_cast<const uint16_t*>(b->v_pool);
+  P.out = static_cast<uint16_t*>(out);
+  const WsLayout L = ws_layout(h, b->num_seqs, b->max_context_len);
+  char* w = static_cast<char*>(const_cast<void*>(ws));
+  P.ws_m = w ? reinterpret_cast<float*>(w + L.m_off) : nullptr;
+  P.ws_z = w ? reinterpret_cast<float*>(w + L.z_off) : nullptr;
+  P.ws_u = w ? reinterpret_cast<float*>(w + L.u_off) : nullptr;
+  P.T = b->total_q_tokens;
+  P.num_pages = b->num_pages;
+  P.num_seqs = b->num_seqs;
+  P.pt_stride = b->pt_stride;
+  P.max_q = b->max_q_len;
+  P.max_ctx = b->max_context_len;
+  P.max_splits = (b->max_context_len + kSplitKeys - 1) / kSplitKeys;
+  P.qtiles = (int)(((int64_t)b->max_q_len * h->group + kChunkCols - 1) / kChunkCols);
+  P.hq = h->hq;
+  P.hkv = h->hkv;
+  P.G = h->group;
+  P.c = h->c;
+  return P;
+}
+
+int launched() { return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH; }
+
+template <int D>
+int run_splits(const vd_attn* h, const Params& P, hipStream_t s, int nb) {
+  const int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
+  const dim3 grid((unsigned)((items + 3) / 4)), block(256);
+  if (nb == 1)
+    hipLaunchKernelGGL((split_kernel<D, 1>), grid, block, 0, s, P);
+  else
+    hipLaunchKernelGGL((split_kernel<D, 2>), grid, block, 0, s, P);
+  return launched();
+}
+
+template <int D>
+int run_merge(const Params& P, hipStream_t s) {
+  hipLaunchKernelGGL((merge_kernel<D>), dim3((unsigned)((int64_t)P.num_seqs * P.hkv)), dim3(256),
+                     0, s, P);
+  return launched();
+}
+
+template <int D>
+int run_chunks(const Params& P, hipStream_t s) {
+  const int64_t blocks = (int64_t)P.num_seqs * P.hkv * P.qtiles;
+  hipLaunchKernelGGL((chunk_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, s, P);
+  return launched();
+}
+
+bool needs_chunks(const vd_attn* h, const vd_attn_batch* b) {
+  return (int64_t)b->max_q_len * h->group > kSplitCols;
+}
+
+}  // namespace
+
+extern "C" {
+
+int vd_attn_create(const vd_attn_desc* desc, vd_attn** out) {
+  if (out) *out = nullptr;
+  if (!desc || !out) return VD_ERR_INVALID_ARG;
+  if (desc->abi_version != VD_ABI_VERSION) return VD_ERR_INVALID_ARG;
+  if (desc->num_q_heads < 1 || desc->num_kv_heads < 1 || desc->head_dim < 1 ||
+      desc->page_size < 1)
+    return VD_ERR_INVALID_ARG;
+  if (desc->dtype != VD_DTYPE_BF16) return VD_ERR_UNSUPPORTED;
+  if (desc->head_dim != 64 && desc->head_dim != 128) return VD_ERR_UNSUPPORTED;
+  if (desc->page_size != kPage) return VD_ERR_UNSUPPORTED;
+  if (desc->num_q_heads % desc->num_kv_heads != 0) return VD_ERR_UNSUPPORTED;
+  if (desc->num_q_heads / desc->num_kv_heads > kSplitCols) return VD_ERR_UNSUPPORTED;
+  if (!(desc->softmax_scale == desc->softmax_scale)) return VD_ERR_INVALID_ARG;  // NaN
+  vd_attn* h = new (std::nothrow) vd_attn;
+  if (!h) return VD_ERR_INVALID_ARG;
+  h->hq = desc->num_q_heads;
+  h->hkv = desc->num_kv_heads;
+  h->d = desc->head_dim;
+  h->page_size = desc->page_size;
+  h->group = desc->num_q_heads / desc->num_kv_heads;
+  const double scale =
+      desc->softmax_scale > 0.0f ? (double)desc->softmax_scale : 1.0 / std::sqrt((double)desc->head_dim);
+  h->scale = (float)scale;
+  h->c = (float)(scale * 1.4426950408889634073599246810019);  // log2(e)
+  *out = h;
+  return VD_OK;
+}
+
+void vd_attn_destroy(vd_attn* h) { delete h; }
+
+int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
+                           int32_t max_context_len, size_t* bytes) {
+  if (!h || !bytes || num_seqs < 0 || max_q_len < 0 || max_context_len < 0)
+    return VD_ERR_INVALID_ARG;
+  (void)max_q_len;
+  *bytes = ws_layout(h, num_seqs, max_context_len).total;
+  return VD_OK;
+}
+
+int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
+  if (!workspace || workspace_bytes < ws_layout(h, b->num_seqs, b->max_context_len).total)
+    return VD_ERR_WORKSPACE;
+  const Params P = make_params(h, b, nullptr, workspace);
+  const int nb = split_nb(h, b->max_q_len);
+  return h->d == 64 ? run_splits<64>(h, P, stream, nb) : run_splits<128>(h, P, stream, nb);
+}
+
+int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* b, void* out,
+                           hipStream_t stream) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
+  if (!out) return VD_ERR_INVALID_ARG;
+  if (!needs_chunks(h, b)) return VD_OK;
+  const Params P = make_params(h, b, out, nullptr);
+  return h->d == 64 ? run_chunks<64>(P, stream) : run_chunks<128>(P, stream);
+}
+
+int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* b, void* out,
+                          const void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
+  if (!out) return VD_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < ws_layout(h, b->num_seqs, b->max_context_len).total)
+    return VD_ERR_WORKSPACE;
+  const Params P = make_params(h, b, out, workspace);
+  return h->d == 64 ? run_merge<64>(P, stream) : run_merge<128>(P, stream);
+}
+
+int vd_attn_forward(const vd_attn* h, const vd_attn_batch* b, void* out, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
+  if (!out) return VD_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < ws_layout(h, b->num_seqs, b->max_context_len).total)
+    return VD_ERR_WORKSPACE;
+  rc = vd_attn_forward_splits(h, b, workspace, workspace_bytes, stream);
+  if (rc != VD_OK) return rc;
+  rc = vd_attn_forward_chunks(h, b, out, stream);
+  if (rc != VD_OK) return rc;
+  return vd_attn_forward_merge(h, b, out, workspace, workspace_bytes, stream);
+}
+
+int vd_pool_bytes(const vd_attn* h, int64_t num_pages, size_t* bytes) {
+  if (!h || !bytes || num_pages < 0) return VD_ERR_INVALID_ARG;
+  *bytes = (size_t)num_pages * h->hkv * kPage * h->d * sizeof(uint16_t);
+  return VD_OK;
+}
+
+int vd_kv_write(const vd_attn* h, const void* k_new, const void* v_new,
+                const int64_t* slot_mapping, int64_t num_tokens, void* k_pool, void* v_pool,
+                int64_t num_pages, hipStream_t stream) {
+  if (!h || num_tokens < 0 || num_pages < 0) return VD_ERR_INVALID_ARG;
+  if (num_tokens == 0) return VD_OK;
+  if (!k_new || !v_new || !slot_mapping || !k_pool || !v_pool) return VD_ERR_INVALID_ARG;
+  const int64_t threads = num_tokens * h->hkv * (h->d / 8);
+  const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+  const uint16_t* kn = static_cast<const uint16_t*>(k_new);
+  const uint16_t* vn = static_cast<const uint16_t*>(v_new);
+  uint16_t* kp = static_cast<uint16_t*>(k_pool);
+  uint16_t* vp = static_cast<uint16_t*>(v_pool);
+  if (h->d == 64)
+    hipLaunchKernelGGL((kv_write_kernel<64>), grid, block, 0, stream, kn, vn, slot_mapping,
+                       num_tokens, kp, vp, num_pages, h->hkv);
+  else
+    hipLaunchKernelGGL((kv_write_kernel<128>), grid, block, 0, stream, kn, vn, slot_mapping,
+                       num_tokens, kp, vp, num_pages, h->hkv);
+  return launched();
+}
+
+const char* vd_status_string(int status) {
+  switch (status) {
+    case VD_OK: return "ok";
+    case VD_ERR_INVALID_ARG: return "invalid argument";
+    case VD_ERR_UNSUPPORTED: return "unsupported configuration";
+    case VD_ERR_WORKSPACE: return "workspace missing or too small";
+    case VD_ERR_LAUNCH: return "kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+int vd_attn_tiling(const vd_attn* h, int32_t* tile_keys, int32_t* split_keys, int32_t* page_size) {
+  if (!h) return VD_ERR_INVALID_ARG;
+  if (tile_keys) *tile_keys = kTileKeys;
+  if (split_keys) *split_keys = kSplitKeys;
+  if (page_size) *page_size = kPage;
+  return VD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,210 @@
+// vd_cas.hpp -- the canonical arithmetic every attention kernel executes.
+//
+// Every kernel of the library computes each output row with exactly the
+// floating-point operations written here, in this order, on operands laid
+// out in registers the same way.  That is the design rule of the paper's
+// Section 3 (the runtime may vary batching, storage and access but must keep
+// each position's floating-point operation sequence) applied to the online
+// softmax update of Appendix A.2 ("A Simplified Tile IR"), plus a split-KV
+// merge in a fixed order.  Compile with -ffp-contract=off: no multiply-add is
+// fused unless written as one.
+//
+// Tiling (fixed per handle, never chosen from the batch):
+//   * key tile     = 64 logical positions = 4 pages of 16
+//   * split        = 512 logical positions (8 tiles); split k covers keys
+//                    [512k, 512k + 512); a row at position p has
+//                    ceil((p + 1) / 512) splits
+//   * dot products = v_mfma_f32_16x16x32_bf16, keys in the M dimension and
+//                    query-head rows ("columns") in the N dimension, D / 32
+//                    instructions chained in ascending d for Q.K and two
+//                    chained in ascending key halves for P.V.
+//
+// Wavefront layout of one 16-column block (lane l, col = l & 15, grp = l >> 4):
+//   Q operand (B of Q.K, chunk ks):  q[col][32 ks + 8 grp + j], j = 0..7
+//   K operand (A of Q.K, page b, ks): K[key 16 b + col][32 ks + 8 grp + j]
+//   score accumulator of page b:     S[key 16 b + 4 grp + i][col], i = 0..3
+//   P operand (B of P.V, half h):    slot j <-> key 32 h + 16 (j / 4) + 4 grp + j % 4
+//   V operand (A of P.V, d-block m, half h): V[that key][16 m + col]
+//   U accumulator of d-block m:      U[16 m + 4 grp + i][col]
+// The MFMA result of one (key, column) or (d, column) cell depends only on
+// its own row of A, column of B and accumulator cell (checked on gfx950:
+// moving a row or column to another slot, or putting NaN in another column,
+// leaves its bits unchanged), so the lane a row lands on does not matter.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vd {
+
+constexpr int kPage = 16;       // tokens per page
+constexpr int kTileKeys = 64;   // keys per online-softmax step
+constexpr int kSplitKeys = 512; // keys per split
+constexpr int kTilesPerSplit = kSplitKeys / kTileKeys;
+constexpr int kPagesPerTile = kTileKeys / kPage;
+constexpr int kSplitCols = 32;  // query-head rows per (request, KV head) on the split path
+constexpr int kChunkCols = 128; // query-head rows per work item on the chunk path
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma(const u16x8& a, const u16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// exp2 of the hardware transcendental unit (v_exp_f32); one function for
+// every kernel.  exp2(-inf) = 0 and exp2(+-0) = 1 exactly.
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// fp32 -> bf16 bits, round to nearest even (inputs here are finite).
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Output cast: bf16 RNE, with -0 mapped to +0 (an all-zero row may carry
+// either sign depending on masked lanes; the canonical output is +0).
+__device__ __forceinline__ uint16_t bf16_out(float f) {
+  uint16_t b = bf16_rne(f);
+  return b == 0x8000u ? (uint16_t)0 : b;
+}
+
+__device__ __forceinline__ float fmax_(float a, float b) { return __builtin_fmaxf(a, b); }
+
+// Cross-lane exchange with lane l ^ mask (mask 16 or 32), via ds_bpermute.
+__device__ __forceinline__ float xor_lane(float v, int mask) {
+  const int lane = __lane_id();
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_ds_bpermute((lane ^ mask) << 2, __builtin_bit_cast(int, v)));
+}
+
+// Online-softmax state of one column (replicated in the 4 lanes of the
+// column): running maximum m, normaliser z, and the D/16 accumulator blocks.
+template <int D>
+struct State {
+  float m, z;
+  f32x4 u[D / 16];
+};
+
+template <int D>
+__device__ __forceinline__ void state_init(State<D>& st) {
+  st.m = -__builtin_inff();
+  st.z = 0.0f;
+#pragma unroll
+  for (int b = 0; b < D / 16; ++b) st.u[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// Score block of one tile for one column block: Q.K over D in ascending
+// 32-wide chunks, one accumulator per page of the tile.
+template <int D>
+__device__ __forceinline__ void tile_scores(const u16x8 (&kf)[kPagesPerTile][D / 32],
+                                            const u16x8 (&qf)[D / 32],
+                                            f32x4 (&acc)[kPagesPerTile]) {
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) a = mfma(kf[b][ks], qf[ks], a);
+    acc[b] = a;
+  }
+}
+
+// One step of Appendix A.2's update for the tile starting at logical key j0,
+// for the column whose position is p (p < 0: padding column, never visible).
+// c is the base-two scale applied to the raw dot.  vf holds the tile's V
+// operands (zero for keys >= n).
+template <int D>
+__device__ __forceinline__ void tile_update(State<D>& st, const f32x4 (&acc)[kPagesPerTile],
+                                            const u16x8 (&vf)[D / 16][2], int j0, int p,
+                                            float c) {
+  const int grp = __lane_id() >> 4;
+  float g[kPagesPerTile][4];
+  bool lam[kPagesPerTile][4];
+  float mx = -__builtin_inff();
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = j0 + 16 * b + 4 * grp + i;
+      lam[b][i] = key <= p;
+      g[b][i] = acc[b][i] * c;
+    }
+  // masked maximum over the tile: fixed tree in the lane, then lanes ^16, ^32
+  float t[kPagesPerTile];
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    const float g0 = lam[b][0] ? g[b][0] : -__builtin_inff();
+    const float g1 = lam[b][1] ? g[b][1] : -__builtin_inff();
+    const float g2 = lam[b][2] ? g[b][2] : -__builtin_inff();
+    const float g3 = lam[b][3] ? g[b][3] : -__builtin_inff();
+    t[b] = fmax_(fmax_(g0, g1), fmax_(g2, g3));
+  }
+  mx = fmax_(fmax_(t[0], t[1]), fmax_(t[2], t[3]));
+  mx = fmax_(mx, xor_lane(mx, 16));
+  mx = fmax_(mx, xor_lane(mx, 32));
+  const bool h = j0 <= p;  // any visible key in this tile for this column
+  const float m_new = fmax_(st.m, mx);
+  // alpha and weights; a column with no visible key keeps its state (select
+  // below), and its operands are zeroed so that nothing non-finite enters
+  // the matrix instruction.
+  const float alpha = h ? ex2(st.m - m_new) : 0.0f;
+  float a[kPagesPerTile][4];
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[b][i] = lam[b][i] ? ex2(g[b][i] - m_new) : 0.0f;
+  // tile sum of the weights: fixed tree in the lane, then lanes ^16, ^32
+  float sb[kPagesPerTile];
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) sb[b] = (a[b][0] + a[b][1]) + (a[b][2] + a[b][3]);
+  float s = (sb[0] + sb[1]) + (sb[2] + sb[3]);
+  s = s + xor_lane(s, 16);
+  s = s + xor_lane(s, 32);
+  const float z_new = st.z * alpha + s;
+  // weights cast to bf16 (the cache type) as the B operand of P.V
+  u16x8 pf[2];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) pf[hh][j] = bf16_rne(a[2 * hh + j / 4][j % 4]);
+#pragma unroll
+  for (int m = 0; m < D / 16; ++m) {
+    f32x4 u = st.u[m] * alpha;
+    u = mfma(vf[m][0], pf[0], u);
+    u = mfma(vf[m][1], pf[1], u);
+    st.u[m] = h ? u : st.u[m];
+  }
+  st.m = h ? m_new : st.m;
+  st.z = h ? z_new : st.z;
+}
+
+// Merge of split partial states in ascending split order (a left fold):
+//   (M, Z, W) <- partial 0;  for k >= 1:
+//   M' = max(M, m_k), a = exp2(M - M'), b = exp2(m_k - M'),
+//   Z <- Z a + z_k b,  W <- W a + U_k b.
+struct FoldScalars {
+  float M, Z, a, b;
+};
+
+__device__ __forceinline__ FoldScalars fold_scalars(float M, float Z, float mk, float zk) {
+  FoldScalars f;
+  const float Mn = fmax_(M, mk);
+  f.a = ex2(M - Mn);
+  f.b = ex2(mk - Mn);
+  f.Z = Z * f.a + zk * f.b;
+  f.M = Mn;
+  return f;
+}
+
+__device__ __forceinline__ float fold_value(float W, float uk, const FoldScalars& f) {
+  return W * f.a + uk * f.b;
+}
+
+// Final normalisation: o = cast(W * select(Z > 0, 1 / Z, 0)), IEEE division.
+__device__ __forceinline__ float final_scale(float Z) { return Z > 0.0f ? 1.0f / Z : 0.0f; }
+
+}  // namespace vd

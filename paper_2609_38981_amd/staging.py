@@ -1,0 +1,71 @@
+"""Moves a synthetic call (``workloads.Call``) to the GPU: device tensors for
+the packed metadata and queries, and pools filled through ``vd_kv_write``.
+
+Pure data movement; the attention itself runs in the library's kernels."""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import workloads as W
+from .vdattn import Batch, VdAttn
+
+
+def bf16_tensor(bits: np.ndarray, device) -> torch.Tensor:
+    """uint16 bf16 bit patterns (numpy) -> torch.bfloat16 on ``device``."""
+    a = np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16)
+    return torch.from_numpy(a).to(device).view(torch.bfloat16)
+
+
+def bits_of(t: torch.Tensor) -> np.ndarray:
+    """torch.bfloat16 -> uint16 bit patterns (numpy, host)."""
+    return t.detach().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+@dataclass
+class DeviceCall:
+    call: W.Call
+    batch: Batch
+
+    @property
+    def kv_bytes(self) -> int:
+        return self.call.kv_bytes()
+
+
+def handle_for(shape: W.Shape) -> VdAttn:
+    return VdAttn(shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.page_size)
+
+
+def fill_pool(attn: VdAttn, call: W.Call, k_pool: torch.Tensor, v_pool: torch.Tensor,
+              chunk_tokens: int = 1 << 16):
+    """Writes every valid slot of ``call`` into the pools with vd_kv_write."""
+    k, v, slots = call.write_list()
+    dev = k_pool.device
+    for lo in range(0, slots.shape[0], chunk_tokens):
+        hi = min(lo + chunk_tokens, slots.shape[0])
+        attn.kv_write(bf16_tensor(k[lo:hi], dev), bf16_tensor(v[lo:hi], dev),
+                      torch.from_numpy(slots[lo:hi]).to(dev), k_pool, v_pool, call.num_pages)
+
+
+def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
+              hint_extra_q: int = 0, hint_extra_ctx: int = 0) -> DeviceCall:
+    """Device copy of ``call``.  Pools start as bf16 NaN (``poison``) or zero,
+    then receive every valid slot; host hints are the call's true maxima plus
+    the given extras."""
+    fill = int(np.int16(np.uint16(W.BF16_QNAN).view(np.int16))) if poison else 0
+    k_pool = attn.new_pool(call.num_pages, device)
+    v_pool = attn.new_pool(call.num_pages, device)
+    k_pool.view(torch.int16).fill_(fill)
+    v_pool.view(torch.int16).fill_(fill)
+    fill_pool(attn, call, k_pool, v_pool)
+    batch = Batch(
+        q=bf16_tensor(call.q_bits(), device),
+        cu_q_lens=torch.from_numpy(call.cu_q_lens).to(device),
+        context_lens=torch.from_numpy(call.context_lens).to(device),
+        page_table=torch.from_numpy(np.ascontiguousarray(call.page_table)).to(device),
+        k_pool=k_pool, v_pool=v_pool, num_pages=call.num_pages,
+        max_q_len=max(call.max_q_len, 1) + hint_extra_q,
+        max_context_len=max(call.max_context_len, 1) + hint_extra_ctx)
+    return DeviceCall(call, batch)

@@ -111,6 +111,7 @@ class Prompt:
     q: np.ndarray
     prefix_key: Optional[int] = None  # identity of a shared prefix, if any
     prefix_len: int = 0
+    tag: Tuple[int, ...] = ()          # identity of the draw: (cfg, pid)
 
     def q_rows(self, lo: int, hi: int) -> np.ndarray:
         assert self.q_lo <= lo <= hi <= self.length, (self.q_lo, lo, hi, self.length)
@@ -135,7 +136,7 @@ def make_prompt(shape: Shape, length: int, cfg: int, pid: int, q_window: Optiona
     v[prefix_len:] = normal_bf16(rng_for(cfg, 3, pid), (own, hkv, d))
     q = normal_bf16(rng_for(cfg, 1, pid), (q_window, hq, d))
     key = id(prefix) if prefix_len else None
-    return Prompt(length, k, v, q_lo, q, key, prefix_len)
+    return Prompt(length, k, v, q_lo, q, key, prefix_len, (cfg, pid))
 
 
 # ---------------------------------------------------------------------------

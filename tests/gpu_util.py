@@ -1,0 +1,99 @@
+"""Helpers of the GPU tests: run a synthetic call through the HIP library and
+through the CPU oracle, and compare rows by logical (prompt, position)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2609_38981_amd import staging as S
+from paper_2609_38981_amd import workloads as W
+from paper_2609_38981_amd.vdattn import VdAttn
+
+# Max abs error allowed against the fp64 oracle for bf16 outputs with fp32
+# accumulation.  Budget: the bf16 cast of the weights before P.V (relative
+# 2^-9 per weight) and the bf16 output rounding (half an ulp, 2^-9 relative,
+# <= 7.8e-3 for |o| < 4) dominate; exp2 and fp32 sums add < 1e-4.
+TOL = 2e-2
+
+
+def say(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU tests need a visible MI355X")
+
+
+_handles = {}
+
+
+def handle(shape: W.Shape) -> VdAttn:
+    if shape not in _handles:
+        _handles[shape] = S.handle_for(shape)
+    return _handles[shape]
+
+
+def gpu_run(call: W.Call, poison: bool = True, stream=None, workspace_fill=None,
+            **kw) -> np.ndarray:
+    """Output bits (uint16 [T, Hq, D]) of one vd_attn_forward call."""
+    attn = handle(call.shape)
+    dc = S.to_device(attn, call, poison=poison, **kw)
+    ws = attn.new_workspace(call.num_seqs, dc.batch.max_q_len, dc.batch.max_context_len)
+    if workspace_fill is not None:
+        ws.view(torch.int8).fill_(workspace_fill)
+    out = torch.empty_like(dc.batch.q)
+    out.view(torch.int16).fill_(0x7FC0)
+    if stream is None:
+        attn.forward(dc.batch, out=out, workspace=ws)
+    else:
+        with torch.cuda.stream(stream):
+            attn.forward(dc.batch, out=out, workspace=ws, stream=stream)
+        stream.synchronize()
+    torch.cuda.synchronize()
+    return S.bits_of(out)
+
+
+def oracle_run(call: W.Call, rows=None) -> np.ndarray:
+    sh = call.shape
+    kp, vp = call.std_pool()
+    return oracle.paged_attention(call.q_bits(), call.cu_q_lens, call.context_lens,
+                                  call.page_table, kp, vp, num_q_heads=sh.num_q_heads,
+                                  num_kv_heads=sh.num_kv_heads, head_dim=sh.head_dim,
+                                  page_size=sh.page_size, rows=rows)
+
+
+def by_position(call: W.Call, out: np.ndarray):
+    """{(prompt identity, position): output row [Hq, D]} for every row."""
+    res = {}
+    for ri, r in enumerate(call.reqs):
+        tag = call.prompts[r.prompt].tag
+        for p in r.positions:
+            res[(tag, p)] = out[call.row_of(ri, p)]
+    return res
+
+
+def parity(call: W.Call, gpu_bits: np.ndarray, rows=None) -> dict:
+    """Compares GPU rows with the oracle; returns error statistics."""
+    ref = oracle_run(call, rows)
+    got = W.bf16_to_f32(gpu_bits).astype(np.float64)
+    sel = np.arange(call.total_q_tokens) if rows is None else np.asarray(rows)
+    diff = np.abs(got[sel] - ref[sel])
+    assert np.isfinite(got[sel]).all(), "non-finite GPU output"
+    st = dict(max_abs=float(diff.max()) if diff.size else 0.0,
+              mean_abs=float(diff.mean()) if diff.size else 0.0, rows=int(len(sel)))
+    assert st["max_abs"] <= TOL, st
+    return st
+
+
+def assert_same_bits(a: dict, b: dict, min_common: int = 1):
+    common = sorted(set(a) & set(b))
+    assert len(common) >= min_common, (len(common), min_common)
+    bad = [k for k in common if not np.array_equal(a[k], b[k])]
+    assert not bad, "bitwise mismatch at %d of %d (prompt, position) rows, e.g. %s" % (
+        len(bad), len(common), bad[:3])
+    return len(common)

@@ -1,0 +1,102 @@
+"""CPU checks of the C ABI: the library loads, exports every function the
+header declares, and rejects bad host-side arguments before any launch.
+Nothing here runs a kernel."""
+from __future__ import annotations
+
+import ctypes
+
+import pytest
+
+from paper_2609_38981_amd import vdattn as V
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return V.load_library()
+
+
+def test_exports_every_declared_function(lib):
+    names = V.declared_functions()
+    assert len(names) >= 11, names
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def _create(lib, **kw):
+    d = dict(abi_version=1, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16, dtype=1,
+             softmax_scale=0.0)
+    d.update(kw)
+    desc = V._Desc(**d)
+    h = ctypes.c_void_p()
+    rc = lib.vd_attn_create(ctypes.byref(desc), ctypes.byref(h))
+    return rc, h
+
+
+def test_create_supported_and_destroy(lib):
+    for hq, hkv, d in [(32, 8, 128), (64, 8, 128), (4, 2, 64), (8, 8, 64)]:
+        rc, h = _create(lib, num_q_heads=hq, num_kv_heads=hkv, head_dim=d)
+        assert rc == 0 and h.value
+        a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        assert lib.vd_attn_tiling(h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == 0
+        assert (a.value, b.value, c.value) == (64, 512, 16)
+        lib.vd_attn_destroy(h)
+    lib.vd_attn_destroy(None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=96), -2), (dict(head_dim=256), -2), (dict(page_size=32), -2),
+    (dict(dtype=2), -2), (dict(num_q_heads=12, num_kv_heads=8), -2),
+    (dict(num_q_heads=64, num_kv_heads=1), -2), (dict(abi_version=2), -1),
+    (dict(num_kv_heads=0), -1), (dict(softmax_scale=float("nan")), -1),
+])
+def test_create_rejects(lib, kw, code):
+    rc, h = _create(lib, **kw)
+    assert rc == code and not h.value
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, 7):
+        assert lib.vd_status_string(code)
+
+
+def test_workspace_and_pool_sizes(lib):
+    rc, h = _create(lib)
+    n = ctypes.c_size_t()
+    assert lib.vd_attn_workspace_size(h, 64, 1, 4096, ctypes.byref(n)) == 0
+    # m, z and U (D floats) per (request, KV head, 32 columns, 8 splits)
+    entries = 64 * 8 * 32 * 8
+    assert n.value >= entries * (2 + 128) * 4
+    assert lib.vd_attn_workspace_size(h, -1, 1, 1, ctypes.byref(n)) == -1
+    assert lib.vd_pool_bytes(h, 10, ctypes.byref(n)) == 0
+    assert n.value == 10 * 8 * 16 * 128 * 2
+    lib.vd_attn_destroy(h)
+
+
+def test_forward_rejects_before_launch(lib):
+    rc, h = _create(lib)
+    fake = 0x1000  # never dereferenced: every case below fails a host check
+    b = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16)
+    ws = ctypes.c_size_t()
+    lib.vd_attn_workspace_size(h, 1, 1, 16, ctypes.byref(ws))
+    # missing workspace / too small
+    assert lib.vd_attn_forward(h, ctypes.byref(b), fake, None, 0, None) == -3
+    assert lib.vd_attn_forward(h, ctypes.byref(b), fake, fake, ws.value - 1, None) == -3
+    # null output
+    assert lib.vd_attn_forward(h, ctypes.byref(b), None, fake, ws.value, None) == -1
+    # null input pointers, bad sizes, inconsistent hints
+    for field, val in [("q", None), ("page_table", None), ("pt_stride", 0), ("num_pages", 0),
+                       ("max_q_len", 0), ("max_context_len", 0), ("num_seqs", -1)]:
+        bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16)
+        setattr(bb, field, val)
+        assert lib.vd_attn_forward(h, ctypes.byref(bb), fake, fake, ws.value, None) == -1, field
+    bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 32, 16)  # max_q > max_ctx
+    assert lib.vd_attn_forward(h, ctypes.byref(bb), fake, fake, ws.value, None) == -1
+    # an empty batch is a no-op
+    e = V._Batch(0, 0, None, None, None, None, 0, None, None, 0, 0, 0)
+    assert lib.vd_attn_forward(h, ctypes.byref(e), None, None, 0, None) == 0
+    assert lib.vd_attn_forward(None, ctypes.byref(e), None, None, 0, None) == -1
+    # kv write
+    assert lib.vd_kv_write(h, fake, fake, fake, -1, fake, fake, 4, None) == -1
+    assert lib.vd_kv_write(h, None, fake, fake, 3, fake, fake, 4, None) == -1
+    assert lib.vd_kv_write(h, fake, fake, fake, 0, fake, fake, 4, None) == 0
+    lib.vd_attn_destroy(h)

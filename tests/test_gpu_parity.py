@@ -1,0 +1,124 @@
+"""GPU parity: the HIP path against the fp64 CPU oracle (max abs error within
+TOL on bf16 outputs), the KV write bit for bit against the documented pool
+layout, and exact closed forms."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_38981_amd import staging as S
+from paper_2609_38981_amd import workloads as W
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    U.require_gpu()
+
+
+# -- a0: the KV write ---------------------------------------------------------
+@pytest.mark.parametrize("shape", [W.TINY, W.LLAMA8B], ids=["d64", "d128"])
+def test_kv_write_layout(shape):
+    U.say("kv_write layout %s" % (shape,))
+    attn = U.handle(shape)
+    rng = np.random.default_rng(5)
+    num_pages, T = 37, 300
+    slots = rng.choice(num_pages * 16, size=T, replace=False).astype(np.int64)
+    slots[7] = -1  # skipped
+    slots[9] = num_pages * 16 + 3  # out of range: skipped
+    k = W.normal_bf16(rng, (T, shape.num_kv_heads, shape.head_dim))
+    v = W.normal_bf16(rng, (T, shape.num_kv_heads, shape.head_dim))
+    kp, vp = attn.new_pool(num_pages), attn.new_pool(num_pages)
+    kp.view(torch.int16).fill_(0x1234)
+    vp.view(torch.int16).fill_(0x1234)
+    attn.kv_write(S.bf16_tensor(k, "cuda"), S.bf16_tensor(v, "cuda"),
+                  torch.from_numpy(slots).cuda(), kp, vp, num_pages)
+    torch.cuda.synchronize()
+    D, H = shape.head_dim, shape.num_kv_heads
+    kb = S.bits_of(kp).reshape(num_pages, H, 16 * D)
+    vb = S.bits_of(vp).reshape(num_pages, H, 16 * D)
+    # decode the layout stated in include/vdattn.h
+    d = np.arange(D)
+    for t in range(T):
+        sl = slots[t]
+        if sl < 0 or sl >= num_pages * 16:
+            continue
+        page, s = sl // 16, sl % 16
+        kidx = ((d // 8) * 16 + s) * 8 + d % 8
+        vidx = ((s // 4) * D + d) * 4 + s % 4
+        assert np.array_equal(kb[page][:, kidx], k[t]), t
+        assert np.array_equal(vb[page][:, vidx], v[t]), t
+    written = set(int(x) for x in slots if 0 <= x < num_pages * 16)
+    untouched = [sl for sl in range(num_pages * 16) if sl not in written][:50]
+    for sl in untouched:
+        page, s = sl // 16, sl % 16
+        assert (kb[page][:, ((d // 8) * 16 + s) * 8 + d % 8] == 0x1234).all()
+
+
+# -- parity against the oracle, sizes the oracle finishes in seconds ----------
+SMALL = {
+    "cfg1_tiny": lambda: W.config1(),
+    "cfg1_tiny_permB": lambda: W.config1(perm_stream=5),
+    "cfg2_decode_small": lambda: W.config2(batch=8, lo=100, hi=1500),
+    "cfg3_mixed_small": lambda: W.config3(num_prefill=2, chunk=40, max_off=700, num_decode=6,
+                                          dec_lo=50, dec_hi=1200),
+    "cfg4_long_small": lambda: W.config4(batch=2, lo=3000, hi=5000),
+    "cfg5_verify_small": lambda: W.config5(num_req=6, prefix=256, suf_lo=20, suf_hi=80),
+    "d64_prefill_chunks": lambda: W.place(W.TINY, [W.make_prompt(W.TINY, 700, 9, 0)],
+                                          [W.Req(0, 700, 700)], W.rng_for(9, 4)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_parity_small(name):
+    call = SMALL[name]()
+    U.say("parity %s: B=%d T=%d max_n=%d" % (name, call.num_seqs, call.total_q_tokens,
+                                             call.max_context_len))
+    out = U.gpu_run(call)
+    st = U.parity(call, out)
+    U.say("  %s" % st)
+
+
+EDGE_LENGTHS = [(1, 1), (2, 1), (16, 1), (17, 1), (63, 1), (64, 1), (65, 1), (511, 1), (512, 1),
+                (513, 1), (1024, 1), (1025, 1), (16, 16), (65, 9), (513, 8), (600, 120),
+                (1100, 1100)]
+
+
+@pytest.mark.parametrize("shape", [W.TINY, W.LLAMA8B, W.LLAMA70B], ids=["tiny", "8b", "70b"])
+def test_parity_edge_lengths(shape):
+    """Ragged tails around page (16), tile (64) and split (512) boundaries, on
+    both the split path (few query rows) and the chunk path (many)."""
+    prompts = [W.make_prompt(shape, n, 8, i, q_window=s) for i, (n, s) in enumerate(EDGE_LENGTHS)]
+    reqs = [W.Req(i, n, s) for i, (n, s) in enumerate(EDGE_LENGTHS)]
+    call = W.place(shape, prompts, reqs, W.rng_for(8, 4))
+    U.say("edge lengths %s T=%d" % (shape, call.total_q_tokens))
+    out = U.gpu_run(call)
+    U.say("  %s" % U.parity(call, out))
+
+
+def test_single_key_is_exact():
+    """n = 1 (and row p = 0 of a whole prefill) returns v_0 bit for bit: one
+    visible key gives weight exp2(0) = 1, z = 1, 1/z = 1."""
+    sh = W.LLAMA8B
+    prompts = [W.make_prompt(sh, 1, 7, 0), W.make_prompt(sh, 40, 7, 1)]
+    call = W.place(sh, prompts, [W.Req(0, 1, 1), W.Req(1, 40, 40)], W.rng_for(7, 4))
+    out = U.gpu_run(call)
+    for ri, pid in [(0, 0), (1, 1)]:
+        row = out[call.row_of(ri, 0)]
+        v0 = prompts[pid].v[0]  # [Hkv, D]
+        for h in range(sh.num_q_heads):
+            assert np.array_equal(row[h], v0[h // sh.group]), (ri, h)
+
+
+def test_parity_full_size_decode_sampled():
+    """Llama-3-8B decode at full size (64 requests, contexts 512..4096): 16
+    sampled rows against the oracle, in the launch configuration the
+    benchmark times."""
+    call = W.config2()
+    U.say("full cfg2: T=%d kv=%.1f MB" % (call.total_q_tokens, call.kv_bytes() / 1e6))
+    out = U.gpu_run(call, poison=False)
+    rows = np.random.default_rng(3).choice(call.total_q_tokens, 16, replace=False)
+    U.say("  %s" % U.parity(call, out, rows=rows))
