@@ -165,7 +165,7 @@ def main():
         attn.forward_splits(b, ws, stream=stream)
         if ev is not None:
             ev[2].record(stream)
-        attn.forward_chunks(b, out, stream=stream)
+        attn.forward_chunks(b, out, ws, stream=stream)
         if ev is not None:
             ev[3].record(stream)
         attn.forward_merge(b, out, ws, stream=stream)

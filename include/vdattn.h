@@ -62,7 +62,7 @@ extern "C" {
 
 typedef enum {
   VD_OK = 0,
-  VD_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad descriptor field */
+  VD_ERR_INVALID_ARG = -1, /* null pointer, negative or oversized size, bad descriptor field */
   VD_ERR_UNSUPPORTED = -2, /* head_dim not in {64, 128}, page_size != 16, dtype != bf16,
                               Hq not a multiple of Hkv, group size > 32; the paper's
                               "reject a missing configuration" (Section 1) */
@@ -109,7 +109,10 @@ typedef struct {
   int32_t max_context_len;      /* HOST hint: >= every n_r (launch sizing only) */
 } vd_attn_batch;
 
-/* Bytes of workspace one call needs for the given host-side sizes. */
+/* Bytes of workspace one call needs for the given host-side sizes: the plan
+ * (three int32 arrays of num_seqs + 1) and, for every (request, KV head,
+ * query-head row < 32, 512-key split < ceil(max_context_len / 512)), a
+ * partial state of head_dim + 2 floats. */
 int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
                            int32_t max_context_len, size_t* bytes);
 
@@ -122,19 +125,21 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, voi
                     size_t workspace_bytes, hipStream_t stream);
 
 /* The three phases vd_attn_forward runs, in this order, for callers that time
- * or schedule them separately (same arguments, same stream, same workspace;
- * their composition is bit-identical to vd_attn_forward):
- *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item per
- *           (request, KV head, 512-key split); writes partial states;
+ * or schedule them separately (same batch, same stream, same workspace; their
+ * composition is bit-identical to vd_attn_forward):
+ *   splits: plans the call (compact work lists in the workspace), then runs
+ *           the rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
+ *           per (request, KV head, 512-key split) -- writing partial states;
  *   chunks: rows of requests with s_r * (Hq / Hkv) > 32 -- one work item per
  *           (request, KV head, 128 query-head rows); folds the splits in
- *           registers and writes their output rows;
+ *           registers and writes their output rows.  Reads the plan written
+ *           by the splits phase of the same batch;
  *   merge:  folds the partial states of the split-phase rows in ascending
  *           split order and writes their output rows. */
 int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* batch, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
 int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* batch, void* out,
-                           hipStream_t stream);
+                           const void* workspace, size_t workspace_bytes, hipStream_t stream);
 int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* batch, void* out,
                           const void* workspace, size_t workspace_bytes, hipStream_t stream);
 
@@ -153,7 +158,7 @@ int vd_pool_bytes(const vd_attn* h, int64_t num_pages, size_t* bytes);
  * Pool layout (one "page block" per (page, KV head), 16 * D bf16 elements at
  * element offset (page * Hkv + kv_head) * 16 * D):
  *   K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
- *   V block: element (slot, d) at ((slot / 4) * D + d) * 4 + slot % 4
+ *   V block: element (slot, d) at ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4
  * so that the matrix-core operand of each wavefront is one contiguous load.
  * Two tokens written to the same slot in one call race (either may win). */
 int vd_kv_write(const vd_attn* h, const void* k_new, const void* v_new,

@@ -1,23 +1,28 @@
 // vd_attn.hip -- HIP kernels for gfx950 and the C ABI of libvdattn.so.
 //
-// Three attention kernels run the canonical arithmetic of vd_cas.hpp:
+// Kernels of one attention call, all on the caller's stream:
+//   plan kernel   one workgroup; reads the per-request lengths and writes
+//                 prefix offsets of three compact work lists into the
+//                 workspace, so that no launched wavefront is idle in the
+//                 middle of the grid (no device-to-host synchronisation).
 //   split kernel  one wavefront per (request, KV head, 512-key split) for
 //                 requests with at most 32 query-head rows per KV head
-//                 (decode, verify); K/V go straight from HBM to registers in
-//                 the matrix-core operand layout; writes a partial state.
-//   merge kernel  folds those partial states in ascending split order and
-//                 writes the output rows.
-//   chunk kernel  one workgroup per (request, KV head, 128 query-head rows)
-//                 for longer chunks (prefill); K/V tiles are staged in LDS
-//                 and shared by the 4 wavefronts; splits are folded in
-//                 registers with the same fold as the merge kernel.
+//                 (decode, verify).  K/V go straight from HBM to registers
+//                 in the matrix-core operand layout; writes a partial state.
+//                 Whole 512-key splits are listed before the shorter last
+//                 splits, so short items fill the end of the launch.
+//   chunk kernel  one workgroup (4 wavefronts x 32 columns) per (request,
+//                 KV head, 128 query-head rows) for longer chunks (prefill);
+//                 K/V tiles are staged in LDS and shared by the wavefronts;
+//                 the splits are folded in registers with the merge's fold.
+//   merge kernel  folds the split partial states in ascending split order
+//                 and writes the output rows of the split-path requests.
 // The work decomposition differs between kernels; the operations applied to
-// any one output row, and their order, do not.
+// any one output row, and their order (vd_cas.hpp), do not.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 #include <cstdint>
-#include <cstdio>
 #include <new>
 
 #include "../../include/vdattn.h"
@@ -35,12 +40,15 @@ struct Params {
   const uint16_t* kpool;
   const uint16_t* vpool;
   uint16_t* out;
+  int32_t* off_full;   // [num_seqs + 1] prefix offsets of whole-split items
+  int32_t* off_part;   // [num_seqs + 1] prefix offsets of last-split items
+  int32_t* off_chunk;  // [num_seqs + 1] prefix offsets of chunk items
   float* ws_m;
   float* ws_z;
   float* ws_u;
   int64_t T;
-  int64_t num_pages;
-  int num_seqs, pt_stride, max_q, max_ctx, max_splits, qtiles;
+  int32_t num_pages;  // page ids are int32: pages past INT32_MAX are unreachable
+  int num_seqs, pt_stride, max_q, max_ctx, max_splits, split_cols;
   int hq, hkv, G;
   float c;  // softmax scale * log2(e), rounded once to fp32 on the host
 };
@@ -64,6 +72,26 @@ __device__ __forceinline__ Req load_req(const Params& P, int r) {
   return R;
 }
 
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Largest r in [0, nseq) with off[r] <= i, for a non-decreasing off[] with
+// off[0] = 0 <= i < off[nseq]: the request whose item range holds item i.
+// 64-ary search, one vector load per level (wave-uniform result).
+__device__ __forceinline__ int find_req(const int32_t* off, int nseq, int i) {
+  const int lane = __lane_id();
+  int lo = 0, hi = nseq;
+  while (hi - lo > 1) {
+    const int step = (hi - lo + 63) / 64;
+    const int cand = lo + lane * step;
+    const bool le = cand < hi && off[cand] <= i;
+    const unsigned long long m = __ballot(le);
+    const int j = 63 - __clzll(m);
+    lo = uni(lo + j * step);
+    hi = uni(min(hi, lo + step));
+  }
+  return lo;
+}
+
 // Index of the (page, kv_head) page block, or -1 when the logical page lp is
 // past the request's keys or its id is outside the pool.
 __device__ __forceinline__ int64_t page_block(const Params& P, const int32_t* ptrow, int lp,
@@ -71,7 +99,7 @@ __device__ __forceinline__ int64_t page_block(const Params& P, const int32_t* pt
   const int npages = (n + kPage - 1) / kPage;
   if (lp >= npages) return -1;
   const int32_t page = ptrow[lp];
-  if (page < 0 || (int64_t)page >= P.num_pages) return -1;
+  if (page < 0 || page >= P.num_pages) return -1;
   return (int64_t)page * P.hkv + g;
 }
 
@@ -81,6 +109,10 @@ __device__ __forceinline__ const uint16_t* block_ptr(const uint16_t* pool, int64
 }
 
 __device__ __forceinline__ u16x8 zero8() { return u16x8{0, 0, 0, 0, 0, 0, 0, 0}; }
+
+__device__ __forceinline__ u16x8 cat4(u16x4 a, u16x4 b) {
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
 
 // Keeps the 4 bf16 values of slots 4 grp .. 4 grp + 3 whose key is < n.
 __device__ __forceinline__ u16x4 mask4(u16x4 v, int key0, int n) {
@@ -100,25 +132,156 @@ __device__ __forceinline__ void load_q(const Params& P, u16x8 (&qf)[D / 32], int
 }
 
 // ---------------------------------------------------------------------------
+// plan kernel: one workgroup of 1024 threads
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(1024) void plan_kernel(Params P) {
+  __shared__ int wsum[3][16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int base[3] = {0, 0, 0};
+  for (int r0 = 0; r0 < P.num_seqs; r0 += 1024) {
+    const int r = r0 + tid;
+    int cnt[3] = {0, 0, 0};
+    if (r < P.num_seqs) {
+      const Req R = load_req(P, r);
+      if (R.valid) {
+        const int ncols = R.s * P.G;
+        if (ncols <= P.split_cols) {
+          cnt[0] = P.hkv * (R.n / kSplitKeys);
+          cnt[1] = (R.n % kSplitKeys) ? P.hkv : 0;
+        } else if (ncols > kSplitCols) {
+          cnt[2] = P.hkv * ((ncols + kChunkCols - 1) / kChunkCols);
+        }
+      }
+    }
+    int incl[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      incl[a] = wave_incl_scan(cnt[a]);
+      if (lane == 63) wsum[a][wave] = incl[a];
+    }
+    __syncthreads();
+    int pre[3] = {0, 0, 0}, tot[3] = {0, 0, 0};
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+      for (int w = 0; w < 16; ++w) {
+        const int v = wsum[a][w];
+        pre[a] += w < wave ? v : 0;
+        tot[a] += v;
+      }
+    if (r < P.num_seqs) {
+      P.off_full[r] = base[0] + pre[0] + incl[0] - cnt[0];
+      P.off_part[r] = base[1] + pre[1] + incl[1] - cnt[1];
+      P.off_chunk[r] = base[2] + pre[2] + incl[2] - cnt[2];
+    }
+#pragma unroll
+    for (int a = 0; a < 3; ++a) base[a] += tot[a];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    P.off_full[P.num_seqs] = base[0];
+    P.off_part[P.num_seqs] = base[1];
+    P.off_chunk[P.num_seqs] = base[2];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // split kernel
 // ---------------------------------------------------------------------------
+// Issue the loads of one tile's K (resp. V) operands.  Every lane loads from
+// a valid page block (a page id that is out of range or past n reads block 0
+// instead), so the load sequence is the same on every tile; the values that
+// must not be used are zeroed afterwards by mask_k / mask_v.
+template <int D>
+__device__ __forceinline__ void load_k(const Params& P, const int64_t (&pb)[kPagesPerTile],
+                                       u16x8 (&kf)[kPagesPerTile][D / 32]) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    const int64_t blk = pb[b] < 0 ? 0 : pb[b];
+    const uint16_t* kb = block_ptr<D>(P.kpool, blk) + 8 * lane;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) kf[b][ks] = *reinterpret_cast<const u16x8*>(kb + 512 * ks);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void load_v(const Params& P, const int64_t (&pb)[kPagesPerTile],
+                                       u16x4 (&vh)[D / 16][kPagesPerTile]) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    const int64_t blk = pb[b] < 0 ? 0 : pb[b];
+    const uint16_t* vb = block_ptr<D>(P.vpool, blk) + 4 * lane;  // = 64 grp + 4 col
+#pragma unroll
+    for (int m = 0; m < D / 16; ++m) vh[m][b] = *reinterpret_cast<const u16x4*>(vb + 256 * m);
+  }
+}
+
+// Zeroes K rows and V entries of keys >= n or of invalid pages (the last,
+// ragged tile of a request only).
+template <int D>
+__device__ __forceinline__ void mask_k(const int64_t (&pb)[kPagesPerTile], int j0, int n,
+                                       u16x8 (&kf)[kPagesPerTile][D / 32]) {
+  const int col = __lane_id() & 15;
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    const bool ok = pb[b] >= 0 && j0 + 16 * b + col < n;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) kf[b][ks] = ok ? kf[b][ks] : zero8();
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void mask_v(const int64_t (&pb)[kPagesPerTile], int j0, int n,
+                                       u16x4 (&vh)[D / 16][kPagesPerTile]) {
+  const int grp = __lane_id() >> 4;
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    const int key0 = j0 + 16 * b + 4 * grp;
+    const bool ok = pb[b] >= 0;
+#pragma unroll
+    for (int m = 0; m < D / 16; ++m)
+      vh[m][b] = ok ? mask4(vh[m][b], key0, n) : u16x4{0, 0, 0, 0};
+  }
+}
+
 template <int D, int NB>
 __global__ __launch_bounds__(256) void split_kernel(Params P) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wave = uni(threadIdx.x >> 6);
   const int lane = __lane_id();
   const int col = lane & 15, grp = lane >> 4;
-  const int64_t item = (int64_t)blockIdx.x * 4 + wave;
-  const int MS = P.max_splits;
-  const int64_t rg = item / MS;
-  const int k = (int)(item % MS);
-  if (rg >= (int64_t)P.num_seqs * P.hkv) return;
-  const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
-  const Req R = load_req(P, r);
-  if (!R.valid) return;
+  const int i = uni(blockIdx.x * 4 + wave);
+  const int tot_full = P.off_full[P.num_seqs], tot_part = P.off_part[P.num_seqs];
+  int r, g, k;
+  Req R;
+  if (i < tot_full) {
+    r = find_req(P.off_full, P.num_seqs, i);
+    R = load_req(P, r);
+    const int local = i - P.off_full[r];
+    const int nfull = R.n / kSplitKeys;
+    g = uni(local / nfull);
+    k = uni(local % nfull);
+  } else if (i < tot_full + tot_part) {
+    const int j = i - tot_full;
+    r = find_req(P.off_part, P.num_seqs, j);
+    R = load_req(P, r);
+    g = uni(j - P.off_part[r]);
+    k = uni(R.n / kSplitKeys);
+  } else {
+    return;
+  }
   const int ncols = R.s * P.G;
-  if (ncols > NB * 16) return;  // chunk path (or a hint violation)
-  const int nsplit = (R.n + kSplitKeys - 1) / kSplitKeys;
-  if (k >= nsplit || nsplit > MS) return;
+  const int MS = P.max_splits;
 
   int pos[NB];
   u16x8 qf[NB][D / 32];
@@ -133,49 +296,40 @@ __global__ __launch_bounds__(256) void split_kernel(Params P) {
   }
 
   const int32_t* ptrow = P.pt + (int64_t)r * P.pt_stride;
-  const int kt_end = min(k * kTilesPerSplit + kTilesPerSplit, (R.n + kTileKeys - 1) / kTileKeys);
-  for (int kt = k * kTilesPerSplit; kt < kt_end; ++kt) {
+  const int kt0 = k * kTilesPerSplit;
+  const int kt_end = min(kt0 + kTilesPerSplit, (R.n + kTileKeys - 1) / kTileKeys);
+  int64_t pb[kPagesPerTile];
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt0 * kPagesPerTile + b, R.n, g);
+  for (int kt = kt0; kt < kt_end; ++kt) {
     const int j0 = kt * kTileKeys;
-    int64_t pb[kPagesPerTile];
-#pragma unroll
-    for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g);
-    // K operands: page b, chunk ks -> 16 contiguous bytes per lane
+    const bool full = j0 + kTileKeys <= R.n && pb[0] >= 0 && pb[1] >= 0 && pb[2] >= 0 && pb[3] >= 0;
     u16x8 kf[kPagesPerTile][D / 32];
+    u16x4 vh[D / 16][kPagesPerTile];
+    load_k<D>(P, pb, kf);
+    // all K loads are issued before the V loads: Q.K can start on them first
+    __builtin_amdgcn_sched_barrier(0);
+    load_v<D>(P, pb, vh);
+    const int64_t pb_cur[kPagesPerTile] = {pb[0], pb[1], pb[2], pb[3]};
+    // page ids of the next tile, while this tile's loads are in flight
 #pragma unroll
-    for (int b = 0; b < kPagesPerTile; ++b) {
-      const bool ok = pb[b] >= 0 && j0 + 16 * b + col < R.n;
-      const uint16_t* base = block_ptr<D>(P.kpool, pb[b] < 0 ? 0 : pb[b]) + 8 * lane;
+    for (int b = 0; b < kPagesPerTile; ++b)
+      pb[b] = page_block(P, ptrow, (kt + 1) * kPagesPerTile + b, R.n, g);
+    if (!full) mask_k<D>(pb_cur, j0, R.n, kf);
+    f32x4 acc[NB][kPagesPerTile];
 #pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks)
-        kf[b][ks] = ok ? *reinterpret_cast<const u16x8*>(base + 512 * ks) : zero8();
-    }
-    // V operands: d-block m, half hh -> 8 bytes from each of two pages
+    for (int nb = 0; nb < NB; ++nb)
+      if (nb * 16 < ncols) tile_scores<D>(kf, qf[nb], acc[nb]);
+    if (!full) mask_v<D>(pb_cur, j0, R.n, vh);
     u16x8 vf[D / 16][2];
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int b = 2 * hh + e;
-        const int key0 = j0 + 16 * b + 4 * grp;
-        const bool ok = pb[b] >= 0 && key0 < R.n;
-        const uint16_t* base =
-            block_ptr<D>(P.vpool, pb[b] < 0 ? 0 : pb[b]) + 4 * (grp * D + col);
-#pragma unroll
-        for (int m = 0; m < D / 16; ++m) {
-          u16x4 v = ok ? *reinterpret_cast<const u16x4*>(base + 64 * m) : u16x4{0, 0, 0, 0};
-          v = mask4(v, key0, R.n);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) vf[m][hh][4 * e + i] = v[i];
-        }
-      }
+    for (int m = 0; m < D / 16; ++m) {
+      vf[m][0] = cat4(vh[m][0], vh[m][1]);
+      vf[m][1] = cat4(vh[m][2], vh[m][3]);
     }
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      if (nb * 16 >= ncols) break;
-      f32x4 acc[kPagesPerTile];
-      tile_scores<D>(kf, qf[nb], acc);
-      tile_update<D>(st[nb], acc, vf, j0, pos[nb], P.c);
-    }
+    for (int nb = 0; nb < NB; ++nb)
+      if (nb * 16 < ncols) tile_update<D>(st[nb], acc[nb], vf, j0, pos[nb], P.c);
   }
 
   // partial state of split k for every column that has a key in it
@@ -205,10 +359,8 @@ __global__ __launch_bounds__(256) void merge_kernel(Params P) {
   const Req R = load_req(P, r);
   if (!R.valid) return;
   const int ncols = R.s * P.G;
-  if (ncols > kSplitCols) return;
-  const int nsplit = (R.n + kSplitKeys - 1) / kSplitKeys;
+  if (ncols > P.split_cols) return;
   const int MS = P.max_splits;
-  if (nsplit > MS) return;
   for (int e = threadIdx.x; e < ncols * (D / 2); e += blockDim.x) {
     const int c = e / (D / 2);
     const int d = 2 * (e % (D / 2));
@@ -243,20 +395,21 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   constexpr int NB = 2;
   constexpr int BLK = kPage * D;  // elements of one page block
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kPagesPerTile][BLK];
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wave = uni(threadIdx.x >> 6);
   const int lane = __lane_id();
   const int col = lane & 15, grp = lane >> 4;
-  const int64_t bid = blockIdx.x;
-  const int qt = (int)(bid % P.qtiles);
-  const int64_t rg = bid / P.qtiles;
-  if (rg >= (int64_t)P.num_seqs * P.hkv) return;
-  const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
+  // blocks of one XCD (block id mod 8) take a contiguous range of items, so
+  // the q-tiles of one (request, KV head) share that XCD's L2
+  const int nb8 = gridDim.x / 8;
+  const int i = uni((int)(blockIdx.x % 8) * nb8 + (int)(blockIdx.x / 8));
+  if (i >= P.off_chunk[P.num_seqs]) return;
+  const int r = find_req(P.off_chunk, P.num_seqs, i);
   const Req R = load_req(P, r);
-  if (!R.valid) return;
   const int ncols = R.s * P.G;
-  if (ncols <= kSplitCols) return;  // split path
+  const int qts = (ncols + kChunkCols - 1) / kChunkCols;
+  const int local = i - P.off_chunk[r];
+  const int g = uni(local / qts), qt = uni(local % qts);
   const int c0 = qt * kChunkCols;
-  if (c0 >= ncols) return;
   const int cend = min(ncols, c0 + kChunkCols);
   const int pmax = R.n - R.s + (cend - 1) / P.G;  // last position of the block
 
@@ -306,7 +459,7 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
             const int slot = (off / 8) % 16;  // K block: [D/8][16][8]
             if (kbase + slot >= R.n) v = zero8();
           } else {
-            const int sg = off / (4 * D);  // V block: [4][D][4]
+            const int sg = (off / 64) % 4;  // V block: [D/16][4][16][4]
 #pragma unroll
             for (int e = 0; e < 8; ++e)
               v[e] = (kbase + 4 * sg + (e % 4) < R.n) ? v[e] : (uint16_t)0;
@@ -326,14 +479,13 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int e = 0; e < 2; ++e)
-#pragma unroll
-          for (int m = 0; m < D / 16; ++m) {
-            const u16x4 v = *reinterpret_cast<const u16x4*>(
-                &lds[kPagesPerTile + 2 * hh + e][4 * (grp * D + 16 * m + col)]);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) vf[m][hh][4 * e + i] = v[i];
-          }
+        for (int m = 0; m < D / 16; ++m) {
+          const u16x4 v0 =
+              *reinterpret_cast<const u16x4*>(&lds[kPagesPerTile + 2 * hh][256 * m + 4 * lane]);
+          const u16x4 v1 =
+              *reinterpret_cast<const u16x4*>(&lds[kPagesPerTile + 2 * hh + 1][256 * m + 4 * lane]);
+          vf[m][hh] = cat4(v0, v1);
+        }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f32x4 acc[kPagesPerTile];
@@ -355,7 +507,7 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
 #pragma unroll
         for (int m = 0; m < D / 16; ++m)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) W[nb][m][i] = fold_value(W[nb][m][i], st[nb].u[m][i], f);
+          for (int e = 0; e < 4; ++e) W[nb][m][e] = fold_value(W[nb][m][e], st[nb].u[m][e], f);
         M[nb] = f.M;
         Z[nb] = f.Z;
       }
@@ -374,7 +526,7 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
     for (int m = 0; m < D / 16; ++m) {
       u16x4 v;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = bf16_out(W[nb][m][i] * rho);
+      for (int e = 0; e < 4; ++e) v[e] = bf16_out(W[nb][m][e] * rho);
       *reinterpret_cast<u16x4*>(o + 16 * m) = v;
     }
   }
@@ -405,9 +557,12 @@ __global__ __launch_bounds__(256) void kv_write_kernel(const uint16_t* knew, con
   const u16x8 vv = *reinterpret_cast<const u16x8*>(vnew + src);
   // K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
   *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + s) * 8) = kv;
-  // V block: element (slot, d) at ((slot / 4) * D + d) * 4 + slot % 4
+  // V block: element (slot, d) at ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4
 #pragma unroll
-  for (int e = 0; e < 8; ++e) vpool[blk + ((int64_t)(s / 4) * D + 8 * dc + e) * 4 + s % 4] = vv[e];
+  for (int e = 0; e < 8; ++e) {
+    const int d = 8 * dc + e;
+    vpool[blk + ((d / 16) * 4 + s / 4) * 64 + (d % 16) * 4 + s % 4] = vv[e];
+  }
 }
 
 }  // namespace
@@ -423,22 +578,24 @@ struct vd_attn {
 
 namespace {
 
-int split_nb(const vd_attn* h, int32_t max_q_len) {
-  return (int64_t)max_q_len * h->group <= 16 ? 1 : 2;
-}
-
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t m_off, z_off, u_off, total;
+  size_t off_full, off_part, off_chunk, m_off, z_off, u_off, total;
 };
 
+// Workspace: three offset arrays of num_seqs + 1 int32, then the split
+// partial states (m, z, U) for every (request, KV head, column < 32, split).
 WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_context_len) {
   const int64_t ms = ((int64_t)max_context_len + kSplitKeys - 1) / kSplitKeys;
   const int64_t n = (int64_t)num_seqs * h->hkv * kSplitCols * (ms < 1 ? 1 : ms);
+  const size_t offs = round_up((size_t)(num_seqs + 1) * sizeof(int32_t));
   WsLayout L;
-  L.m_off = 0;
-  L.z_off = round_up(n * sizeof(float));
+  L.off_full = 0;
+  L.off_part = offs;
+  L.off_chunk = 2 * offs;
+  L.m_off = 3 * offs;
+  L.z_off = L.m_off + round_up(n * sizeof(float));
   L.u_off = L.z_off + round_up(n * sizeof(float));
   L.total = L.u_off + round_up((size_t)n * h->d * sizeof(float));
   return L;
@@ -453,7 +610,12 @@ int check_batch(const vd_attn* h, const vd_attn_batch* b) {
   if (b->pt_stride < 1 || b->num_pages < 1 || b->max_q_len < 1 || b->max_context_len < 1)
     return VD_ERR_INVALID_ARG;
   if (b->max_q_len > b->max_context_len) return VD_ERR_INVALID_ARG;
+  if (b->total_q_tokens > INT32_MAX) return VD_ERR_INVALID_ARG;
   return VD_OK;
+}
+
+int split_nb(const vd_attn* h, int32_t max_q_len) {
+  return (int64_t)max_q_len * h->group <= 16 ? 1 : 2;
 }
 
 Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const void* ws) {
@@ -467,17 +629,20 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.out = static_cast<uint16_t*>(out);
   const WsLayout L = ws_layout(h, b->num_seqs, b->max_context_len);
   char* w = static_cast<char*>(const_cast<void*>(ws));
-  P.ws_m = w ? reinterpret_cast<float*>(w + L.m_off) : nullptr;
-  P.ws_z = w ? reinterpret_cast<float*>(w + L.z_off) : nullptr;
-  P.ws_u = w ? reinterpret_cast<float*>(w + L.u_off) : nullptr;
+  P.off_full = reinterpret_cast<int32_t*>(w + L.off_full);
+  P.off_part = reinterpret_cast<int32_t*>(w + L.off_part);
+  P.off_chunk = reinterpret_cast<int32_t*>(w + L.off_chunk);
+  P.ws_m = reinterpret_cast<float*>(w + L.m_off);
+  P.ws_z = reinterpret_cast<float*>(w + L.z_off);
+  P.ws_u = reinterpret_cast<float*>(w + L.u_off);
   P.T = b->total_q_tokens;
-  P.num_pages = b->num_pages;
+  P.num_pages = (int32_t)(b->num_pages > INT32_MAX ? INT32_MAX : b->num_pages);
   P.num_seqs = b->num_seqs;
   P.pt_stride = b->pt_stride;
   P.max_q = b->max_q_len;
   P.max_ctx = b->max_context_len;
   P.max_splits = (b->max_context_len + kSplitKeys - 1) / kSplitKeys;
-  P.qtiles = (int)(((int64_t)b->max_q_len * h->group + kChunkCols - 1) / kChunkCols);
+  P.split_cols = 16 * split_nb(h, b->max_q_len);
   P.hq = h->hq;
   P.hkv = h->hkv;
   P.G = h->group;
@@ -488,10 +653,13 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
 int launched() { return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH; }
 
 template <int D>
-int run_splits(const vd_attn* h, const Params& P, hipStream_t s, int nb) {
+int run_splits(const Params& P, hipStream_t s) {
+  // upper bound of the split items; items past the planned total exit at once
   const int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
+  if (items > INT32_MAX - 4) return VD_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, P);
   const dim3 grid((unsigned)((items + 3) / 4)), block(256);
-  if (nb == 1)
+  if (P.split_cols == 16)
     hipLaunchKernelGGL((split_kernel<D, 1>), grid, block, 0, s, P);
   else
     hipLaunchKernelGGL((split_kernel<D, 2>), grid, block, 0, s, P);
@@ -507,13 +675,21 @@ int run_merge(const Params& P, hipStream_t s) {
 
 template <int D>
 int run_chunks(const Params& P, hipStream_t s) {
-  const int64_t blocks = (int64_t)P.num_seqs * P.hkv * P.qtiles;
+  // upper bound of sum_r Hkv * ceil(s_r G / 128) <= Hkv (ceil(T G / 128) + B),
+  // rounded up to a multiple of the 8 XCDs
+  int64_t blocks = (int64_t)P.hkv * ((P.T * P.G + kChunkCols - 1) / kChunkCols + P.num_seqs);
+  blocks = (blocks + 7) / 8 * 8;
+  if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
   hipLaunchKernelGGL((chunk_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, s, P);
   return launched();
 }
 
 bool needs_chunks(const vd_attn* h, const vd_attn_batch* b) {
   return (int64_t)b->max_q_len * h->group > kSplitCols;
+}
+
+bool ws_ok(const vd_attn* h, const vd_attn_batch* b, const void* ws, size_t bytes) {
+  return ws && bytes >= ws_layout(h, b->num_seqs, b->max_context_len).total;
 }
 
 }  // namespace
@@ -527,12 +703,12 @@ int vd_attn_create(const vd_attn_desc* desc, vd_attn** out) {
   if (desc->num_q_heads < 1 || desc->num_kv_heads < 1 || desc->head_dim < 1 ||
       desc->page_size < 1)
     return VD_ERR_INVALID_ARG;
+  if (!(desc->softmax_scale == desc->softmax_scale)) return VD_ERR_INVALID_ARG;  // NaN
   if (desc->dtype != VD_DTYPE_BF16) return VD_ERR_UNSUPPORTED;
   if (desc->head_dim != 64 && desc->head_dim != 128) return VD_ERR_UNSUPPORTED;
   if (desc->page_size != kPage) return VD_ERR_UNSUPPORTED;
   if (desc->num_q_heads % desc->num_kv_heads != 0) return VD_ERR_UNSUPPORTED;
   if (desc->num_q_heads / desc->num_kv_heads > kSplitCols) return VD_ERR_UNSUPPORTED;
-  if (!(desc->softmax_scale == desc->softmax_scale)) return VD_ERR_INVALID_ARG;  // NaN
   vd_attn* h = new (std::nothrow) vd_attn;
   if (!h) return VD_ERR_INVALID_ARG;
   h->hq = desc->num_q_heads;
@@ -540,8 +716,8 @@ int vd_attn_create(const vd_attn_desc* desc, vd_attn** out) {
   h->d = desc->head_dim;
   h->page_size = desc->page_size;
   h->group = desc->num_q_heads / desc->num_kv_heads;
-  const double scale =
-      desc->softmax_scale > 0.0f ? (double)desc->softmax_scale : 1.0 / std::sqrt((double)desc->head_dim);
+  const double scale = desc->softmax_scale > 0.0f ? (double)desc->softmax_scale
+                                                  : 1.0 / std::sqrt((double)desc->head_dim);
   h->scale = (float)scale;
   h->c = (float)(scale * 1.4426950408889634073599246810019);  // log2(e)
   *out = h;
@@ -554,7 +730,6 @@ int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len
                            int32_t max_context_len, size_t* bytes) {
   if (!h || !bytes || num_seqs < 0 || max_q_len < 0 || max_context_len < 0)
     return VD_ERR_INVALID_ARG;
-  (void)max_q_len;
   *bytes = ws_layout(h, num_seqs, max_context_len).total;
   return VD_OK;
 }
@@ -563,20 +738,19 @@ int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* works
                            size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
-  if (!workspace || workspace_bytes < ws_layout(h, b->num_seqs, b->max_context_len).total)
-    return VD_ERR_WORKSPACE;
+  if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, nullptr, workspace);
-  const int nb = split_nb(h, b->max_q_len);
-  return h->d == 64 ? run_splits<64>(h, P, stream, nb) : run_splits<128>(h, P, stream, nb);
+  return h->d == 64 ? run_splits<64>(P, stream) : run_splits<128>(P, stream);
 }
 
 int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* b, void* out,
-                           hipStream_t stream) {
+                           const void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
   if (!out) return VD_ERR_INVALID_ARG;
+  if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   if (!needs_chunks(h, b)) return VD_OK;
-  const Params P = make_params(h, b, out, nullptr);
+  const Params P = make_params(h, b, out, workspace);
   return h->d == 64 ? run_chunks<64>(P, stream) : run_chunks<128>(P, stream);
 }
 
@@ -585,8 +759,7 @@ int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* b, void* out,
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
   if (!out) return VD_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < ws_layout(h, b->num_seqs, b->max_context_len).total)
-    return VD_ERR_WORKSPACE;
+  if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
   return h->d == 64 ? run_merge<64>(P, stream) : run_merge<128>(P, stream);
 }
@@ -596,11 +769,10 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* b, void* out, void* w
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
   if (!out) return VD_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < ws_layout(h, b->num_seqs, b->max_context_len).total)
-    return VD_ERR_WORKSPACE;
+  if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   rc = vd_attn_forward_splits(h, b, workspace, workspace_bytes, stream);
   if (rc != VD_OK) return rc;
-  rc = vd_attn_forward_chunks(h, b, out, stream);
+  rc = vd_attn_forward_chunks(h, b, out, workspace, workspace_bytes, stream);
   if (rc != VD_OK) return rc;
   return vd_attn_forward_merge(h, b, out, workspace, workspace_bytes, stream);
 }

@@ -72,7 +72,7 @@ def load_library(path: str = LIB_PATH):
         "vd_attn_workspace_size": (ctypes.c_int, [P, I32, I32, I32, ctypes.POINTER(SZ)]),
         "vd_attn_forward": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_attn_forward_splits": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, SZ, P]),
-        "vd_attn_forward_chunks": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P]),
+        "vd_attn_forward_chunks": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_attn_forward_merge": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_pool_bytes": (ctypes.c_int, [P, I64, ctypes.POINTER(SZ)]),
         "vd_kv_write": (ctypes.c_int, [P, P, P, P, I64, P, P, I64, P]),
@@ -242,11 +242,13 @@ class VdAttn:
         _check(self.lib.vd_attn_forward_splits(self._h, ctypes.byref(cb), _ptr(ws), ws.numel(),
                                                _stream(stream)), "vd_attn_forward_splits")
 
-    def forward_chunks(self, b: Batch, out, stream=None):
+    def forward_chunks(self, b: Batch, out, workspace, stream=None):
         cb = self._batch(b)
         out = self._out(b, out)
-        _check(self.lib.vd_attn_forward_chunks(self._h, ctypes.byref(cb), _ptr(out),
-                                               _stream(stream)), "vd_attn_forward_chunks")
+        ws = self._ws(b, workspace)
+        _check(self.lib.vd_attn_forward_chunks(self._h, ctypes.byref(cb), _ptr(out), _ptr(ws),
+                                               ws.numel(), _stream(stream)),
+               "vd_attn_forward_chunks")
 
     def forward_merge(self, b: Batch, out, workspace, stream=None):
         cb = self._batch(b)

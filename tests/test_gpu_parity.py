@@ -48,7 +48,7 @@ def test_kv_write_layout(shape):
             continue
         page, s = sl // 16, sl % 16
         kidx = ((d // 8) * 16 + s) * 8 + d % 8
-        vidx = ((s // 4) * D + d) * 4 + s % 4
+        vidx = ((d // 16) * 4 + s // 4) * 64 + (d % 16) * 4 + s % 4
         assert np.array_equal(kb[page][:, kidx], k[t]), t
         assert np.array_equal(vb[page][:, vidx], v[t]), t
     written = set(int(x) for x in slots if 0 <= x < num_pages * 16)
