@@ -124,20 +124,26 @@ int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len
 int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
 
-/* The three phases vd_attn_forward runs, in this order, for callers that time
- * or schedule them separately (same batch, same stream, same workspace; their
- * composition is bit-identical to vd_attn_forward):
- *   splits: plans the call (compact work lists in the workspace), then runs
- *           the rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
- *           per (request, KV head, 512-key split) -- writing partial states;
+/* The four phases vd_attn_forward runs, in this order, for callers that time
+ * or schedule them separately (same batch, same output, same stream, same
+ * workspace; their composition is bit-identical to vd_attn_forward):
+ *   plan:   reads the per-request lengths on the device and writes the
+ *           compact work lists of the split and chunk phases into the
+ *           workspace (no device-to-host synchronisation);
+ *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
+ *           per (request, KV head, 512-key split).  A request with one split
+ *           writes its output rows directly; otherwise each item writes a
+ *           partial state;
  *   chunks: rows of requests with s_r * (Hq / Hkv) > 32 -- one work item per
  *           (request, KV head, 128 query-head rows); folds the splits in
- *           registers and writes their output rows.  Reads the plan written
- *           by the splits phase of the same batch;
- *   merge:  folds the partial states of the split-phase rows in ascending
- *           split order and writes their output rows. */
-int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* batch, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream);
+ *           registers and writes their output rows;
+ *   merge:  folds the partial states of the split-phase rows of requests
+ *           with more than one split, in ascending split order, and writes
+ *           their output rows. */
+int vd_attn_forward_plan(const vd_attn* h, const vd_attn_batch* batch, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* batch, void* out,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream);
 int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* batch, void* out,
                            const void* workspace, size_t workspace_bytes, hipStream_t stream);
 int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* batch, void* out,

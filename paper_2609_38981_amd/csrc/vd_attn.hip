@@ -21,6 +21,7 @@
 // any one output row, and their order (vd_cas.hpp), do not.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <new>
@@ -129,6 +130,22 @@ __device__ __forceinline__ void load_q(const Params& P, u16x8 (&qf)[D / 32], int
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks)
     qf[ks] = valid ? *reinterpret_cast<const u16x8*>(base + 32 * ks) : zero8();
+}
+
+// Stores one column's output row from its accumulator blocks (lane layout of
+// the U accumulator: d = 16 m + 4 grp + i).
+template <int D>
+__device__ __forceinline__ void store_row(const Params& P, const f32x4 (&u)[D / 16], float rho,
+                                          int64_t tok, int head) {
+  const int grp = __lane_id() >> 4;
+  uint16_t* o = P.out + (tok * P.hq + head) * D + 4 * grp;
+#pragma unroll
+  for (int m = 0; m < D / 16; ++m) {
+    u16x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = bf16_out(u[m][i] * rho);
+    *reinterpret_cast<u16x4*>(o + 16 * m) = v;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -332,6 +349,17 @@ __global__ __launch_bounds__(256) void split_kernel(Params P) {
       if (nb * 16 < ncols) tile_update<D>(st[nb], acc[nb], vf, j0, pos[nb], P.c);
   }
 
+  const int nsplit = (R.n - 1) / kSplitKeys + 1;
+  if (nsplit == 1) {
+    // a single split: the merged state is this state; normalise and store
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      if (pos[nb] < 0) continue;
+      const int c = nb * 16 + col;
+      store_row<D>(P, st[nb].u, final_scale(st[nb].z), R.q0 + c / P.G, g * P.G + c % P.G);
+    }
+    return;
+  }
   // partial state of split k for every column that has a key in it
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -349,40 +377,96 @@ __global__ __launch_bounds__(256) void split_kernel(Params P) {
 }
 
 // ---------------------------------------------------------------------------
-// merge kernel: one workgroup per (request, KV head)
+// merge kernel: one workgroup of 256 threads per
+// (request, KV head, slice of 256 output elements).  The fold is the same left
+// fold as fold_scalars / fold_value, evaluated in 64-split chunks: the running
+// maximum is an exact prefix maximum, so the two exp2 factors of every step
+// are computed in parallel; the Z and W recurrences stay sequential in k.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void merge_kernel(Params P) {
-  const int64_t rg = blockIdx.x;
+__global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
+  constexpr int CH = 64;
+  constexpr int SC = 256 / D + 1;  // columns a slice can touch
+  __shared__ float sa[SC][CH], sb[SC][CH], sz[SC][CH];
+  __shared__ float sM[SC], sZ[SC];
+  const int64_t bid = blockIdx.x;
+  const int slice = (int)(bid % slices);
+  const int64_t rg = bid / slices;
   if (rg >= (int64_t)P.num_seqs * P.hkv) return;
   const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
   const Req R = load_req(P, r);
   if (!R.valid) return;
   const int ncols = R.s * P.G;
   if (ncols > P.split_cols) return;
+  const int nsplit = (R.n - 1) / kSplitKeys + 1;
+  if (nsplit == 1) return;  // written by the split kernel
+  const int e0 = slice * 256;
+  if (e0 >= ncols * D) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cfirst = e0 / D;
+  const int clast = (min(ncols * D, e0 + 256) - 1) / D;
+  const int ncs = clast - cfirst + 1;
   const int MS = P.max_splits;
-  for (int e = threadIdx.x; e < ncols * (D / 2); e += blockDim.x) {
-    const int c = e / (D / 2);
-    const int d = 2 * (e % (D / 2));
-    const int pos = R.n - R.s + c / P.G;
-    const int kp = pos / kSplitKeys + 1;
-    const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS;
-    float M = P.ws_m[p0], Z = P.ws_z[p0];
-    float2 W = *reinterpret_cast<const float2*>(P.ws_u + p0 * D + d);
-    for (int k = 1; k < kp; ++k) {
-      const FoldScalars f = fold_scalars(M, Z, P.ws_m[p0 + k], P.ws_z[p0 + k]);
-      const float2 uk = *reinterpret_cast<const float2*>(P.ws_u + (p0 + k) * D + d);
-      W.x = fold_value(W.x, uk.x, f);
-      W.y = fold_value(W.y, uk.y, f);
-      M = f.M;
-      Z = f.Z;
+  const int64_t base = (int64_t)(r * P.hkv + g) * kSplitCols * MS;
+  const int e = e0 + tid;
+  const bool mine = e < ncols * D;
+  const int c = mine ? e / D : cfirst;
+  const int d = e % D;
+  const int kp = (R.n - R.s + c / P.G) / kSplitKeys + 1;
+  const int64_t pu = (base + (int64_t)c * MS) * D + d;
+  float W = 0.f;
+  for (int k0 = 0; k0 < nsplit; k0 += CH) {
+    // per-column factors of this chunk: wavefront w takes columns w, w + 4, ...
+    for (int ci = wave; ci < ncs; ci += 4) {
+      const int cc = cfirst + ci;
+      const int kpc = (R.n - R.s + cc / P.G) / kSplitKeys + 1;
+      const int64_t p0 = base + (int64_t)cc * MS;
+      const int k = k0 + lane;
+      const bool has = k < kpc;
+      const float mk = has ? P.ws_m[p0 + k] : -__builtin_inff();
+      const float zk = has ? P.ws_z[p0 + k] : 0.0f;
+      const float carry = k0 == 0 ? -__builtin_inff() : sM[ci];
+      float pm = mk;  // inclusive prefix maximum over the chunk
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const float t = __shfl_up(pm, o, 64);
+        if (lane >= o) pm = fmax_(pm, t);
+      }
+      const float Mk = fmax_(carry, pm);
+      float Mp = __shfl_up(Mk, 1, 64);
+      if (lane == 0) Mp = carry;
+      sa[ci][lane] = ex2(Mp - Mk);
+      sb[ci][lane] = ex2(mk - Mk);
+      sz[ci][lane] = zk;
+      const float Mlast = __shfl(Mk, 63, 64);
+      if (lane == 0) {
+        // Z recurrence of this chunk (sequential, as fold_scalars)
+        float Z = k0 == 0 ? zk : sZ[ci];
+        const int kend = min(CH, kpc - k0);
+        for (int kk = k0 == 0 ? 1 : 0; kk < kend; ++kk) Z = Z * sa[ci][kk] + sz[ci][kk] * sb[ci][kk];
+        sZ[ci] = Z;
+        sM[ci] = Mlast;
+      }
     }
-    const float rho = final_scale(Z);
-    const int64_t tok = R.q0 + c / P.G;
-    const int head = g * P.G + c % P.G;
-    uint16_t* o = P.out + (tok * P.hq + head) * D + d;
-    const uint32_t packed = (uint32_t)bf16_out(W.x * rho) | ((uint32_t)bf16_out(W.y * rho) << 16);
-    *reinterpret_cast<uint32_t*>(o) = packed;
+    __syncthreads();
+    if (mine) {
+      const int kend = min(CH, kp - k0);
+      const int ci = c - cfirst;
+      float u[CH];
+#pragma unroll
+      for (int kk = 0; kk < CH; ++kk) u[kk] = kk < kend ? P.ws_u[pu + (int64_t)(k0 + kk) * D] : 0.0f;
+      if (k0 == 0) W = u[0];
+      const int kbeg = k0 == 0 ? 1 : 0;
+#pragma unroll
+      for (int kk = 0; kk < CH; ++kk)
+        if (kk >= kbeg && kk < kend)
+          W = fold_value(W, u[kk], FoldScalars{0.f, 0.f, sa[ci][kk], sb[ci][kk]});
+    }
+    __syncthreads();
+  }
+  if (mine) {
+    const float rho = final_scale(sZ[c - cfirst]);
+    P.out[((int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G) * D + d] = bf16_out(W * rho);
   }
 }
 
@@ -518,17 +602,7 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   for (int nb = 0; nb < NB; ++nb) {
     if (pos[nb] < 0) continue;
     const int c = c0 + wave * 32 + nb * 16 + col;
-    const float rho = final_scale(Z[nb]);
-    const int64_t tok = R.q0 + c / P.G;
-    const int head = g * P.G + c % P.G;
-    uint16_t* o = P.out + (tok * P.hq + head) * D + 4 * grp;
-#pragma unroll
-    for (int m = 0; m < D / 16; ++m) {
-      u16x4 v;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = bf16_out(W[nb][m][e] * rho);
-      *reinterpret_cast<u16x4*>(o + 16 * m) = v;
-    }
+    store_row<D>(P, W[nb], final_scale(Z[nb]), R.q0 + c / P.G, g * P.G + c % P.G);
   }
 }
 
@@ -579,6 +653,7 @@ struct vd_attn {
 namespace {
 
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
 
 struct WsLayout {
   size_t off_full, off_part, off_chunk, m_off, z_off, u_off, total;
@@ -652,12 +727,18 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
 
 int launched() { return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH; }
 
+
+
+int run_plan(const Params& P, hipStream_t s) {
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, P);
+  return launched();
+}
+
 template <int D>
 int run_splits(const Params& P, hipStream_t s) {
   // upper bound of the split items; items past the planned total exit at once
   const int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
   if (items > INT32_MAX - 4) return VD_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, P);
   const dim3 grid((unsigned)((items + 3) / 4)), block(256);
   if (P.split_cols == 16)
     hipLaunchKernelGGL((split_kernel<D, 1>), grid, block, 0, s, P);
@@ -668,8 +749,11 @@ int run_splits(const Params& P, hipStream_t s) {
 
 template <int D>
 int run_merge(const Params& P, hipStream_t s) {
-  hipLaunchKernelGGL((merge_kernel<D>), dim3((unsigned)((int64_t)P.num_seqs * P.hkv)), dim3(256),
-                     0, s, P);
+  const int64_t cols = std::min<int64_t>((int64_t)P.max_q * P.G, P.split_cols);
+  const int slices = (int)((cols * D + 255) / 256);
+  const int64_t blocks = (int64_t)P.num_seqs * P.hkv * slices;
+  if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
+  hipLaunchKernelGGL((merge_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, s, P, slices);
   return launched();
 }
 
@@ -734,12 +818,21 @@ int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len
   return VD_OK;
 }
 
-int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
+int vd_attn_forward_plan(const vd_attn* h, const vd_attn_batch* b, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
-  const Params P = make_params(h, b, nullptr, workspace);
+  return run_plan(make_params(h, b, nullptr, workspace), stream);
+}
+
+int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* out, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
+  if (!out) return VD_ERR_INVALID_ARG;
+  if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
+  const Params P = make_params(h, b, out, workspace);
   return h->d == 64 ? run_splits<64>(P, stream) : run_splits<128>(P, stream);
 }
 
@@ -770,7 +863,9 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* b, void* out, void* w
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
   if (!out) return VD_ERR_INVALID_ARG;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
-  rc = vd_attn_forward_splits(h, b, workspace, workspace_bytes, stream);
+  rc = vd_attn_forward_plan(h, b, workspace, workspace_bytes, stream);
+  if (rc != VD_OK) return rc;
+  rc = vd_attn_forward_splits(h, b, out, workspace, workspace_bytes, stream);
   if (rc != VD_OK) return rc;
   rc = vd_attn_forward_chunks(h, b, out, workspace, workspace_bytes, stream);
   if (rc != VD_OK) return rc;

@@ -71,7 +71,8 @@ def load_library(path: str = LIB_PATH):
         "vd_attn_destroy": (None, [P]),
         "vd_attn_workspace_size": (ctypes.c_int, [P, I32, I32, I32, ctypes.POINTER(SZ)]),
         "vd_attn_forward": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
-        "vd_attn_forward_splits": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, SZ, P]),
+        "vd_attn_forward_plan": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, SZ, P]),
+        "vd_attn_forward_splits": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_attn_forward_chunks": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_attn_forward_merge": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_pool_bytes": (ctypes.c_int, [P, I64, ctypes.POINTER(SZ)]),
@@ -236,11 +237,19 @@ class VdAttn:
                                         _stream(stream)), "vd_attn_forward")
         return out
 
-    def forward_splits(self, b: Batch, workspace, stream=None):
+    def forward_plan(self, b: Batch, workspace, stream=None):
         cb = self._batch(b)
         ws = self._ws(b, workspace)
-        _check(self.lib.vd_attn_forward_splits(self._h, ctypes.byref(cb), _ptr(ws), ws.numel(),
-                                               _stream(stream)), "vd_attn_forward_splits")
+        _check(self.lib.vd_attn_forward_plan(self._h, ctypes.byref(cb), _ptr(ws), ws.numel(),
+                                             _stream(stream)), "vd_attn_forward_plan")
+
+    def forward_splits(self, b: Batch, out, workspace, stream=None):
+        cb = self._batch(b)
+        out = self._out(b, out)
+        ws = self._ws(b, workspace)
+        _check(self.lib.vd_attn_forward_splits(self._h, ctypes.byref(cb), _ptr(out), _ptr(ws),
+                                               ws.numel(), _stream(stream)),
+               "vd_attn_forward_splits")
 
     def forward_chunks(self, b: Batch, out, workspace, stream=None):
         cb = self._batch(b)

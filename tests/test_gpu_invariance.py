@@ -107,6 +107,7 @@ def test_metadata_does_not_matter():
     call = mk()
     variants = {
         "hints": dict(hint_extra_q=7, hint_extra_ctx=3000),
+        "hints_long": dict(hint_extra_ctx=20000),
         "ws_nan": dict(workspace_fill=-1),
         "stream": dict(stream=torch.cuda.Stream()),
         "repeat": {},

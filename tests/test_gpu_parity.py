@@ -66,6 +66,8 @@ SMALL = {
     "cfg3_mixed_small": lambda: W.config3(num_prefill=2, chunk=40, max_off=700, num_decode=6,
                                           dec_lo=50, dec_hi=1200),
     "cfg4_long_small": lambda: W.config4(batch=2, lo=3000, hi=5000),
+    # over 64 splits per request: several merge chunks
+    "cfg4_long_mid": lambda: W.config4(batch=3, lo=9000, hi=40000),
     "cfg5_verify_small": lambda: W.config5(num_req=6, prefix=256, suf_lo=20, suf_hi=80),
     "d64_prefill_chunks": lambda: W.place(W.TINY, [W.make_prompt(W.TINY, 700, 9, 0)],
                                           [W.Req(0, 700, 700)], W.rng_for(9, 4)),
