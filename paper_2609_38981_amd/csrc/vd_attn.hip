@@ -99,7 +99,9 @@ __device__ __forceinline__ int64_t page_block(const Params& P, const int32_t* pt
                                               int n, int g) {
   const int npages = (n + kPage - 1) / kPage;
   if (lp >= npages) return -1;
-  const int32_t page = ptrow[lp];
+  // the page table is read-only for the whole call: a scalar load
+  typedef __attribute__((address_space(4))) const int32_t const_i32;
+  const int32_t page = ((const_i32*)ptrow)[lp];
   if (page < 0 || page >= P.num_pages) return -1;
   return (int64_t)page * P.hkv + g;
 }
@@ -110,6 +112,9 @@ __device__ __forceinline__ const uint16_t* block_ptr(const uint16_t* pool, int64
 }
 
 __device__ __forceinline__ u16x8 zero8() { return u16x8{0, 0, 0, 0, 0, 0, 0, 0}; }
+
+// Tile kt lies wholly below key n.
+__device__ __forceinline__ bool j0_full(int kt, int n) { return (kt + 1) * kTileKeys <= n; }
 
 __device__ __forceinline__ u16x8 cat4(u16x4 a, u16x4 b) {
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -272,39 +277,20 @@ __device__ __forceinline__ void mask_v(const int64_t (&pb)[kPagesPerTile], int j
   }
 }
 
-template <int D, int NB>
-__global__ __launch_bounds__(256) void split_kernel(Params P) {
-  const int wave = uni(threadIdx.x >> 6);
+// One split item: the tiles of split k of request r, KV head g, for NA
+// column blocks of 16 query-head rows.
+template <int D, int NA>
+__device__ __forceinline__ void split_item(const Params& P, int r, int g, int k, const Req& R) {
   const int lane = __lane_id();
   const int col = lane & 15, grp = lane >> 4;
-  const int i = uni(blockIdx.x * 4 + wave);
-  const int tot_full = P.off_full[P.num_seqs], tot_part = P.off_part[P.num_seqs];
-  int r, g, k;
-  Req R;
-  if (i < tot_full) {
-    r = find_req(P.off_full, P.num_seqs, i);
-    R = load_req(P, r);
-    const int local = i - P.off_full[r];
-    const int nfull = R.n / kSplitKeys;
-    g = uni(local / nfull);
-    k = uni(local % nfull);
-  } else if (i < tot_full + tot_part) {
-    const int j = i - tot_full;
-    r = find_req(P.off_part, P.num_seqs, j);
-    R = load_req(P, r);
-    g = uni(j - P.off_part[r]);
-    k = uni(R.n / kSplitKeys);
-  } else {
-    return;
-  }
   const int ncols = R.s * P.G;
   const int MS = P.max_splits;
 
-  int pos[NB];
-  u16x8 qf[NB][D / 32];
-  State<D> st[NB];
+  int pos[NA];
+  u16x8 qf[NA][D / 32];
+  State<D> st[NA];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
+  for (int nb = 0; nb < NA; ++nb) {
     const int c = nb * 16 + col;
     const bool v = c < ncols;
     pos[nb] = v ? R.n - R.s + c / P.G : -1;
@@ -333,27 +319,27 @@ __global__ __launch_bounds__(256) void split_kernel(Params P) {
     for (int b = 0; b < kPagesPerTile; ++b)
       pb[b] = page_block(P, ptrow, (kt + 1) * kPagesPerTile + b, R.n, g);
     if (!full) mask_k<D>(pb_cur, j0, R.n, kf);
-    f32x4 acc[NB][kPagesPerTile];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      if (nb * 16 < ncols) tile_scores<D>(kf, qf[nb], acc[nb]);
+    f32x4 acc[NA][kPagesPerTile];
+    tile_scores<D, NA>([&](int b, int ks) { return kf[b][ks]; }, qf, acc);
     if (!full) mask_v<D>(pb_cur, j0, R.n, vh);
-    u16x8 vf[D / 16][2];
+    TileWeights w[NA];
+#pragma unroll
+    for (int nb = 0; nb < NA; ++nb) w[nb] = tile_softmax<D>(st[nb], acc[nb], j0, pos[nb], P.c);
 #pragma unroll
     for (int m = 0; m < D / 16; ++m) {
-      vf[m][0] = cat4(vh[m][0], vh[m][1]);
-      vf[m][1] = cat4(vh[m][2], vh[m][3]);
+      const u16x8 v0 = cat4(vh[m][0], vh[m][1]), v1 = cat4(vh[m][2], vh[m][3]);
+#pragma unroll
+      for (int nb = 0; nb < NA; ++nb) tile_pv_block<D>(st[nb], w[nb], m, v0, v1);
     }
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      if (nb * 16 < ncols) tile_update<D>(st[nb], acc[nb], vf, j0, pos[nb], P.c);
+    for (int nb = 0; nb < NA; ++nb) tile_commit<D>(st[nb], w[nb]);
   }
 
   const int nsplit = (R.n - 1) / kSplitKeys + 1;
   if (nsplit == 1) {
     // a single split: the merged state is this state; normalise and store
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+    for (int nb = 0; nb < NA; ++nb) {
       if (pos[nb] < 0) continue;
       const int c = nb * 16 + col;
       store_row<D>(P, st[nb].u, final_scale(st[nb].z), R.q0 + c / P.G, g * P.G + c % P.G);
@@ -362,7 +348,7 @@ __global__ __launch_bounds__(256) void split_kernel(Params P) {
   }
   // partial state of split k for every column that has a key in it
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
+  for (int nb = 0; nb < NA; ++nb) {
     const int c = nb * 16 + col;
     if (pos[nb] < 0 || k > pos[nb] / kSplitKeys) continue;
     const int64_t pidx = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS + k;
@@ -374,6 +360,75 @@ __global__ __launch_bounds__(256) void split_kernel(Params P) {
 #pragma unroll
     for (int m = 0; m < D / 16; ++m) *reinterpret_cast<f32x4*>(u + 16 * m) = st[nb].u[m];
   }
+}
+
+template <int D, int NB>
+__global__ __launch_bounds__(256) void split_kernel(Params P) {
+  const int wave = uni(threadIdx.x >> 6);
+  const int i = uni(blockIdx.x * 4 + wave);
+  const int tot_full = P.off_full[P.num_seqs], tot_part = P.off_part[P.num_seqs];
+  int r, g, k;
+  Req R;
+  if (i < tot_full) {
+    r = find_req(P.off_full, P.num_seqs, i);
+    R = load_req(P, r);
+    const int local = i - P.off_full[r];
+    const int nfull = R.n / kSplitKeys;
+    g = uni(local / nfull);
+    k = uni(local % nfull);
+  } else if (i < tot_full + tot_part) {
+    const int j = i - tot_full;
+    r = find_req(P.off_part, P.num_seqs, j);
+    R = load_req(P, r);
+    g = uni(j - P.off_part[r]);
+    k = uni(R.n / kSplitKeys);
+  } else {
+    return;
+  }
+  // column blocks actually used by this request: one wave-uniform dispatch
+  if (NB == 2 && R.s * P.G > 16)
+    split_item<D, NB>(P, r, g, k, R);
+  else
+    split_item<D, 1>(P, r, g, k, R);
+}
+
+// ---------------------------------------------------------------------------
+// short merge (contexts of at most 16 splits): one thread per (request, KV
+// head, column, 4 consecutive d), folding the partial states in ascending
+// split order with fold_scalars / fold_value.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int per_rg = cols * (D / 4);
+  const int64_t rg = id / per_rg;
+  if (rg >= (int64_t)P.num_seqs * P.hkv) return;
+  const int rem = (int)(id % per_rg);
+  const int c = rem / (D / 4), d = 4 * (rem % (D / 4));
+  const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
+  const Req R = load_req(P, r);
+  if (!R.valid) return;
+  const int ncols = R.s * P.G;
+  if (ncols > P.split_cols || c >= ncols) return;
+  if ((R.n - 1) / kSplitKeys == 0) return;  // one split: written by the split kernel
+  const int MS = P.max_splits;
+  const int kp = (R.n - R.s + c / P.G) / kSplitKeys + 1;
+  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS;
+  float M = P.ws_m[p0], Z = P.ws_z[p0];
+  f32x4 W = *reinterpret_cast<const f32x4*>(P.ws_u + p0 * D + d);
+  for (int k = 1; k < kp; ++k) {
+    const FoldScalars f = fold_scalars(M, Z, P.ws_m[p0 + k], P.ws_z[p0 + k]);
+    const f32x4 uk = *reinterpret_cast<const f32x4*>(P.ws_u + (p0 + k) * D + d);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) W[i] = fold_value(W[i], uk[i], f);
+    M = f.M;
+    Z = f.Z;
+  }
+  const float rho = final_scale(Z);
+  u16x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = bf16_out(W[i] * rho);
+  *reinterpret_cast<u16x4*>(P.out + ((int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G) * D + d) = o;
 }
 
 // ---------------------------------------------------------------------------
@@ -472,21 +527,63 @@ __global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
 
 // ---------------------------------------------------------------------------
 // chunk kernel: one workgroup (4 wavefronts x 32 columns) per
-// (request, KV head, 128 query-head rows); K/V tiles staged in LDS.
+// (request, KV head, 128 query-head rows).  The request's K/V tiles stream
+// through a 3-stage LDS ring filled by direct global-to-LDS loads: while the
+// wavefronts compute tile t, the loads of tiles t + 1 and t + 2 are in
+// flight.  The splits are folded in registers as each one ends.
 // ---------------------------------------------------------------------------
+// Direct global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
+// byte address m0val + 16 l.  Issued as inline assembly so that the compiler
+// does not make every later LDS read wait for all such copies; the kernel
+// waits for them itself with wait_vmcnt.  M0 is saved and restored.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0val) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(m0val)
+      : "memory");
+}
+
+// Workgroup barrier that orders LDS accesses only (global memory operations
+// in flight are not waited for).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   constexpr int NB = 2;
-  constexpr int BLK = kPage * D;  // elements of one page block
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kPagesPerTile][BLK];
+  constexpr int BLK = kPage * D;                   // elements of one page block
+  constexpr int NBLK = 2 * kPagesPerTile;          // 4 K blocks then 4 V blocks
+  constexpr int TILE = NBLK * BLK;                 // elements of one staged tile
+  constexpr int WCH = TILE / (4 * 512);            // 1 KB copies per wavefront per tile
+  constexpr int STAGES = 3;
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];  // [STAGES][NBLK][BLK]
   const int wave = uni(threadIdx.x >> 6);
   const int lane = __lane_id();
-  const int col = lane & 15, grp = lane >> 4;
-  // blocks of one XCD (block id mod 8) take a contiguous range of items, so
-  // the q-tiles of one (request, KV head) share that XCD's L2
-  const int nb8 = gridDim.x / 8;
-  const int i = uni((int)(blockIdx.x % 8) * nb8 + (int)(blockIdx.x / 8));
-  if (i >= P.off_chunk[P.num_seqs]) return;
+  const int col = lane & 15;
+  // Blocks of one XCD (block id mod 8) take a contiguous range of the items
+  // so that the q-tiles of one (request, KV head) share that XCD's L2.
+  const int total = P.off_chunk[P.num_seqs];
+  const int per_xcd = (total + 7) / 8;
+  const int jx = (int)(blockIdx.x / 8);
+  if (jx >= per_xcd) return;
+  const int i = uni((int)(blockIdx.x % 8) * per_xcd + jx);
+  if (i >= total) return;
   const int r = find_req(P.off_chunk, P.num_seqs, i);
   const Req R = load_req(P, r);
   const int ncols = R.s * P.G;
@@ -509,8 +606,9 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
     const bool v = c < cend;
     pos[nb] = v ? R.n - R.s + c / P.G : -1;
     load_q<D>(P, qf[nb], R.q0 + (v ? c / P.G : 0), g * P.G + (v ? c % P.G : 0), v);
-    const int clast = min(cend, c0 + wave * 32 + nb * 16 + 16) - 1;
-    if (clast >= c0 + wave * 32 + nb * 16) wave_pmax = max(wave_pmax, R.n - R.s + clast / P.G);
+    const int cb = c0 + wave * 32 + nb * 16;
+    const int clast = min(cend, cb + 16) - 1;
+    if (clast >= cb) wave_pmax = max(wave_pmax, R.n - R.s + clast / P.G);
     M[nb] = 0.f;
     Z[nb] = 0.f;
 #pragma unroll
@@ -518,82 +616,122 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   }
 
   const int32_t* ptrow = P.pt + (int64_t)r * P.pt_stride;
-  const int nsplit = pmax / kSplitKeys + 1;
   const int ntiles = pmax / kTileKeys + 1;
-  for (int k = 0; k < nsplit; ++k) {
+  // Issues this wavefront's WCH direct loads of tile kt into stage buf: copy
+  // q = wave * WCH + w moves 1 KB of page block q / (BLK / 512).
+  auto fetch = [&](int kt, int buf) {
+    int64_t pb[kPagesPerTile];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) state_init(st[nb]);
-    const int kt_end = min(k * kTilesPerSplit + kTilesPerSplit, ntiles);
-    for (int kt = k * kTilesPerSplit; kt < kt_end; ++kt) {
-      const int j0 = kt * kTileKeys;
-      __syncthreads();  // the previous tile's readers are done
-      // cooperative copy: 8 page blocks (4 K, 4 V) of BLK elements, 16 B per step
-      for (int ch = threadIdx.x; ch < 2 * kPagesPerTile * (BLK / 8); ch += blockDim.x) {
-        const int blk = ch / (BLK / 8);
-        const int off = (ch % (BLK / 8)) * 8;
-        const int b = blk % kPagesPerTile;
-        const bool isv = blk >= kPagesPerTile;
-        const int64_t pb = page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g);
-        const int kbase = j0 + 16 * b;
-        u16x8 v = zero8();
-        if (pb >= 0) {
-          const uint16_t* src = block_ptr<D>(isv ? P.vpool : P.kpool, pb) + off;
-          v = *reinterpret_cast<const u16x8*>(src);
-          if (!isv) {
-            const int slot = (off / 8) % 16;  // K block: [D/8][16][8]
-            if (kbase + slot >= R.n) v = zero8();
-          } else {
-            const int sg = (off / 64) % 4;  // V block: [D/16][4][16][4]
+    for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g);
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              v[e] = (kbase + 4 * sg + (e % 4) < R.n) ? v[e] : (uint16_t)0;
-          }
-        }
-        *reinterpret_cast<u16x8*>(&lds[blk][off]) = v;
+    for (int w = 0; w < WCH; ++w) {
+      const int q = wave * WCH + w;
+      const int blk = q / (BLK / 512), sub = q % (BLK / 512);
+      const int b = blk % kPagesPerTile;
+      const int64_t pbb = pb[b] < 0 ? 0 : pb[b];
+      const uint16_t* src =
+          block_ptr<D>(blk < kPagesPerTile ? P.kpool : P.vpool, pbb) + 512 * sub + 8 * lane;
+      const uint32_t dst = (uint32_t)(uintptr_t)(lds + (buf * NBLK + blk) * BLK + 512 * sub);
+      lds_dma16(src, uni((int)dst));
+    }
+  };
+  // Zeroes, in stage buf, the K rows and V entries of keys >= n or of
+  // invalid pages (a request's last, ragged tile only).
+  auto mask_stage = [&](int kt, int buf) {
+    const int j0 = kt * kTileKeys;
+    bool pvalid[kPagesPerTile];
+#pragma unroll
+    for (int b = 0; b < kPagesPerTile; ++b)
+      pvalid[b] = page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g) >= 0;
+    for (int ch = threadIdx.x; ch < TILE / 8; ch += 256) {
+      const int blk = ch / (BLK / 8), off = (ch % (BLK / 8)) * 8;
+      const int b = blk % kPagesPerTile;
+      const int kbase = j0 + 16 * b;
+      const bool pok = pvalid[b];
+      u16x8* p = reinterpret_cast<u16x8*>(lds + (buf * NBLK + blk) * BLK + off);
+      u16x8 v = *p;
+      if (blk < kPagesPerTile) {
+        const int slot = (off / 8) % 16;  // K block: [D/8][16][8]
+        if (!pok || kbase + slot >= R.n) v = zero8();
+      } else {
+        const int sg = (off / 64) % 4;  // V block: [D/16][4][16][4]
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (pok && kbase + 4 * sg + (e % 4) < R.n) ? v[e] : (uint16_t)0;
       }
-      __syncthreads();
-      if (wave_pmax < j0) continue;  // no column of this wave sees the tile
-      u16x8 kf[kPagesPerTile][D / 32];
+      *p = v;
+    }
+  };
+  auto tile_is_full = [&](int kt) {
+    if ((kt + 1) * kTileKeys > R.n) return false;
 #pragma unroll
-      for (int b = 0; b < kPagesPerTile; ++b)
+    for (int b = 0; b < kPagesPerTile; ++b)
+      if (page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g) < 0) return false;
+    return true;
+  };
+
+  wait_vmcnt<0>();  // the Q operands are in registers before any tile copy is issued
+  fetch(0, 0);
+  if (ntiles > 1) fetch(1, 1);
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int j0 = kt * kTileKeys;
+    const int k = kt / kTilesPerSplit;
+    const int buf = kt % STAGES;
+    // tile kt has landed once at most the next tile's loads are outstanding
+    if (kt + 1 < ntiles)
+      wait_vmcnt<WCH>();
+    else
+      wait_vmcnt<0>();
+    lds_barrier();  // every wavefront's part of tile kt is in LDS; tile kt - 1 is consumed
+    if (!tile_is_full(kt)) {
+      mask_stage(kt, buf);
+      lds_barrier();
+    }
+    if (kt + 2 < ntiles) fetch(kt + 2, (kt + 2) % STAGES);
+    if (kt % kTilesPerSplit == 0) {
 #pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks)
-          kf[b][ks] = *reinterpret_cast<const u16x8*>(&lds[b][512 * ks + 8 * lane]);
-      u16x8 vf[D / 16][2];
+      for (int nb = 0; nb < NB; ++nb) state_init(st[nb]);
+    }
+    const uint16_t* T = lds + buf * NBLK * BLK;
+    if (wave_pmax >= j0) {
+      f32x4 acc[NB][kPagesPerTile];
+      tile_scores<D, NB>(
+          [&](int b, int ks) { return *reinterpret_cast<const u16x8*>(T + b * BLK + 512 * ks + 8 * lane); },
+          qf, acc);
+      TileWeights w[NB];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
+      for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D>(st[nb], acc[nb], j0, pos[nb], P.c);
 #pragma unroll
-        for (int m = 0; m < D / 16; ++m) {
-          const u16x4 v0 =
-              *reinterpret_cast<const u16x4*>(&lds[kPagesPerTile + 2 * hh][256 * m + 4 * lane]);
-          const u16x4 v1 =
-              *reinterpret_cast<const u16x4*>(&lds[kPagesPerTile + 2 * hh + 1][256 * m + 4 * lane]);
-          vf[m][hh] = cat4(v0, v1);
-        }
+      for (int m = 0; m < D / 16; ++m) {
+        const int o = 256 * m + 4 * lane;
+        const u16x8 v0 = cat4(*reinterpret_cast<const u16x4*>(T + 4 * BLK + o),
+                              *reinterpret_cast<const u16x4*>(T + 5 * BLK + o));
+        const u16x8 v1 = cat4(*reinterpret_cast<const u16x4*>(T + 6 * BLK + o),
+                              *reinterpret_cast<const u16x4*>(T + 7 * BLK + o));
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) tile_pv_block<D>(st[nb], w[nb], m, v0, v1);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) tile_commit<D>(st[nb], w[nb]);
+    }
+    if (kt % kTilesPerSplit == kTilesPerSplit - 1 || kt == ntiles - 1) {
+      // split k ends: fold it into the running merge for columns that have it
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        f32x4 acc[kPagesPerTile];
-        tile_scores<D>(kf, qf[nb], acc);
-        tile_update<D>(st[nb], acc, vf, j0, pos[nb], P.c);
-      }
-    }
-    // fold split k into the running merge for columns that have it
+        if (pos[nb] < 0 || k > pos[nb] / kSplitKeys) continue;
+        if (k == 0) {
+          M[nb] = st[nb].m;
+          Z[nb] = st[nb].z;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      if (pos[nb] < 0 || k > pos[nb] / kSplitKeys) continue;
-      if (k == 0) {
-        M[nb] = st[nb].m;
-        Z[nb] = st[nb].z;
+          for (int m = 0; m < D / 16; ++m) W[nb][m] = st[nb].u[m];
+        } else {
+          const FoldScalars f = fold_scalars(M[nb], Z[nb], st[nb].m, st[nb].z);
 #pragma unroll
-        for (int m = 0; m < D / 16; ++m) W[nb][m] = st[nb].u[m];
-      } else {
-        const FoldScalars f = fold_scalars(M[nb], Z[nb], st[nb].m, st[nb].z);
+          for (int m = 0; m < D / 16; ++m)
 #pragma unroll
-        for (int m = 0; m < D / 16; ++m)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) W[nb][m][e] = fold_value(W[nb][m][e], st[nb].u[m][e], f);
-        M[nb] = f.M;
-        Z[nb] = f.Z;
+            for (int e = 0; e < 4; ++e) W[nb][m][e] = fold_value(W[nb][m][e], st[nb].u[m][e], f);
+          M[nb] = f.M;
+          Z[nb] = f.Z;
+        }
       }
     }
   }
@@ -604,6 +742,12 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
     const int c = c0 + wave * 32 + nb * 16 + col;
     store_row<D>(P, W[nb], final_scale(Z[nb]), R.q0 + c / P.G, g * P.G + c % P.G);
   }
+}
+
+// Dynamic LDS bytes of the chunk kernel: 3 stages of 8 page blocks.
+template <int D>
+constexpr size_t chunk_lds_bytes() {
+  return (size_t)3 * 2 * kPagesPerTile * kPage * D * sizeof(uint16_t);
 }
 
 // ---------------------------------------------------------------------------
@@ -747,9 +891,21 @@ int run_splits(const Params& P, hipStream_t s) {
   return launched();
 }
 
+// Up to this many splits per request the short merge (one thread per output
+// quad, sequential fold) is used; beyond it the chunked merge kernel.
+constexpr int kShortMergeSplits = 16;
+
 template <int D>
 int run_merge(const Params& P, hipStream_t s) {
   const int64_t cols = std::min<int64_t>((int64_t)P.max_q * P.G, P.split_cols);
+  if (P.max_splits <= kShortMergeSplits) {
+    const int64_t threads = (int64_t)P.num_seqs * P.hkv * cols * (D / 4);
+    const int64_t blocks = (threads + 255) / 256;
+    if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
+    hipLaunchKernelGGL((merge_short_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, s, P,
+                       (int)cols);
+    return launched();
+  }
   const int slices = (int)((cols * D + 255) / 256);
   const int64_t blocks = (int64_t)P.num_seqs * P.hkv * slices;
   if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
@@ -764,7 +920,12 @@ int run_chunks(const Params& P, hipStream_t s) {
   int64_t blocks = (int64_t)P.hkv * ((P.T * P.G + kChunkCols - 1) / kChunkCols + P.num_seqs);
   blocks = (blocks + 7) / 8 * 8;
   if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
-  hipLaunchKernelGGL((chunk_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, s, P);
+  constexpr size_t lds = chunk_lds_bytes<D>();
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&chunk_kernel<D>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)lds);
+  if (attr != hipSuccess) return VD_ERR_LAUNCH;
+  hipLaunchKernelGGL((chunk_kernel<D>), dim3((unsigned)blocks), dim3(256), lds, s, P);
   return launched();
 }
 

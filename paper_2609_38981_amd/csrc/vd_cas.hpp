@@ -98,33 +98,45 @@ __device__ __forceinline__ void state_init(State<D>& st) {
   for (int b = 0; b < D / 16; ++b) st.u[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
-// Score block of one tile for one column block: Q.K over D in ascending
-// 32-wide chunks, one accumulator per page of the tile.
-template <int D>
-__device__ __forceinline__ void tile_scores(const u16x8 (&kf)[kPagesPerTile][D / 32],
-                                            const u16x8 (&qf)[D / 32],
-                                            f32x4 (&acc)[kPagesPerTile]) {
+// Score blocks of one tile for NB column blocks: Q.K over D in ascending
+// 32-wide chunks, one accumulator chain per (column block, page).  kf(b, ks)
+// yields the K operand of page b, chunk ks; a K operand is shared by the
+// column blocks, each chain is independent.
+template <int D, int NB, class KF>
+__device__ __forceinline__ void tile_scores(const KF& kf, const u16x8 (&qf)[NB][D / 32],
+                                            f32x4 (&acc)[NB][kPagesPerTile]) {
 #pragma unroll
-  for (int b = 0; b < kPagesPerTile; ++b) {
-    f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) a = mfma(kf[b][ks], qf[ks], a);
-    acc[b] = a;
-  }
+    for (int b = 0; b < kPagesPerTile; ++b) acc[nb][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b)
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const u16x8 k = kf(b, ks);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb][b] = mfma(k, qf[nb][ks], acc[nb][b]);
+    }
 }
 
-// One step of Appendix A.2's update for the tile starting at logical key j0,
-// for the column whose position is p (p < 0: padding column, never visible).
-// c is the base-two scale applied to the raw dot.  vf holds the tile's V
-// operands (zero for keys >= n).
+// Softmax half of Appendix A.2's update for the tile starting at logical key
+// j0, for the column at position p (p < 0: a padding column, never visible);
+// c is the base-two scale applied to the raw dot.  Produces the weights (cast
+// to bf16, the cache type, as the B operand of P.V), alpha, and the candidate
+// (m, z); h says whether the column sees any key of the tile.
+struct TileWeights {
+  u16x8 pf[2];
+  float alpha, m_new, z_new;
+  bool h;
+};
+
 template <int D>
-__device__ __forceinline__ void tile_update(State<D>& st, const f32x4 (&acc)[kPagesPerTile],
-                                            const u16x8 (&vf)[D / 16][2], int j0, int p,
-                                            float c) {
+__device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
+                                                    const f32x4 (&acc)[kPagesPerTile], int j0,
+                                                    int p, float c) {
   const int grp = __lane_id() >> 4;
   float g[kPagesPerTile][4];
   bool lam[kPagesPerTile][4];
-  float mx = -__builtin_inff();
 #pragma unroll
   for (int b = 0; b < kPagesPerTile; ++b)
 #pragma unroll
@@ -143,20 +155,20 @@ __device__ __forceinline__ void tile_update(State<D>& st, const f32x4 (&acc)[kPa
     const float g3 = lam[b][3] ? g[b][3] : -__builtin_inff();
     t[b] = fmax_(fmax_(g0, g1), fmax_(g2, g3));
   }
-  mx = fmax_(fmax_(t[0], t[1]), fmax_(t[2], t[3]));
+  float mx = fmax_(fmax_(t[0], t[1]), fmax_(t[2], t[3]));
   mx = fmax_(mx, xor_lane(mx, 16));
   mx = fmax_(mx, xor_lane(mx, 32));
-  const bool h = j0 <= p;  // any visible key in this tile for this column
-  const float m_new = fmax_(st.m, mx);
-  // alpha and weights; a column with no visible key keeps its state (select
-  // below), and its operands are zeroed so that nothing non-finite enters
-  // the matrix instruction.
-  const float alpha = h ? ex2(st.m - m_new) : 0.0f;
+  TileWeights w;
+  w.h = j0 <= p;  // any visible key in this tile for this column
+  w.m_new = fmax_(st.m, mx);
+  // A column with no visible key keeps its state (tile_commit), and its
+  // operands are zeroed so that nothing non-finite enters the matrix core.
+  w.alpha = w.h ? ex2(st.m - w.m_new) : 0.0f;
   float a[kPagesPerTile][4];
 #pragma unroll
   for (int b = 0; b < kPagesPerTile; ++b)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[b][i] = lam[b][i] ? ex2(g[b][i] - m_new) : 0.0f;
+    for (int i = 0; i < 4; ++i) a[b][i] = lam[b][i] ? ex2(g[b][i] - w.m_new) : 0.0f;
   // tile sum of the weights: fixed tree in the lane, then lanes ^16, ^32
   float sb[kPagesPerTile];
 #pragma unroll
@@ -164,22 +176,30 @@ __device__ __forceinline__ void tile_update(State<D>& st, const f32x4 (&acc)[kPa
   float s = (sb[0] + sb[1]) + (sb[2] + sb[3]);
   s = s + xor_lane(s, 16);
   s = s + xor_lane(s, 32);
-  const float z_new = st.z * alpha + s;
-  // weights cast to bf16 (the cache type) as the B operand of P.V
-  u16x8 pf[2];
+  w.z_new = st.z * w.alpha + s;
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) pf[hh][j] = bf16_rne(a[2 * hh + j / 4][j % 4]);
-#pragma unroll
-  for (int m = 0; m < D / 16; ++m) {
-    f32x4 u = st.u[m] * alpha;
-    u = mfma(vf[m][0], pf[0], u);
-    u = mfma(vf[m][1], pf[1], u);
-    st.u[m] = h ? u : st.u[m];
-  }
-  st.m = h ? m_new : st.m;
-  st.z = h ? z_new : st.z;
+    for (int j = 0; j < 8; ++j) w.pf[hh][j] = bf16_rne(a[2 * hh + j / 4][j % 4]);
+  return w;
+}
+
+// P.V for d-block m: U <- dot(bf16(A), V, U * alpha), keys in two 32-wide
+// halves in ascending order (v0: keys 0-31 of the tile, v1: keys 32-63).
+template <int D>
+__device__ __forceinline__ void tile_pv_block(State<D>& st, const TileWeights& w, int m,
+                                              const u16x8& v0, const u16x8& v1) {
+  f32x4 u = st.u[m] * w.alpha;
+  u = mfma(v0, w.pf[0], u);
+  u = mfma(v1, w.pf[1], u);
+  st.u[m] = w.h ? u : st.u[m];
+}
+
+// (m, z) <- select(h, new, old)
+template <int D>
+__device__ __forceinline__ void tile_commit(State<D>& st, const TileWeights& w) {
+  st.m = w.h ? w.m_new : st.m;
+  st.z = w.h ? w.z_new : st.z;
 }
 
 // Merge of split partial states in ascending split order (a left fold):
