@@ -43,7 +43,7 @@ struct Params {
   uint16_t* out;
   int32_t* off_full;   // [num_seqs + 1] prefix offsets of whole-split items
   int32_t* off_part;   // [num_seqs + 1] prefix offsets of last-split items
-  int32_t* off_chunk;  // [num_seqs + 1] prefix offsets of chunk items
+  int32_t* off_chunk;  // [num_seqs + 1] prefix offsets of q-tiles (per KV head)
   float* ws_m;
   float* ws_z;
   float* ws_u;
@@ -181,7 +181,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
           cnt[0] = P.hkv * (R.n / kSplitKeys);
           cnt[1] = (R.n % kSplitKeys) ? P.hkv : 0;
         } else if (ncols > kSplitCols) {
-          cnt[2] = P.hkv * ((ncols + kChunkCols - 1) / kChunkCols);
+          cnt[2] = (ncols + kChunkCols - 1) / kChunkCols;  // q-tiles per KV head
         }
       }
     }
@@ -323,8 +323,16 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     tile_scores<D, NA>([&](int b, int ks) { return kf[b][ks]; }, qf, acc);
     if (!full) mask_v<D>(pb_cur, j0, R.n, vh);
     TileWeights w[NA];
+    bool open = true;  // every key of the tile visible to every column
 #pragma unroll
-    for (int nb = 0; nb < NA; ++nb) w[nb] = tile_softmax<D>(st[nb], acc[nb], j0, pos[nb], P.c);
+    for (int nb = 0; nb < NA; ++nb) open = open && __all(pos[nb] >= j0 + kTileKeys - 1);
+    if (open) {
+#pragma unroll
+      for (int nb = 0; nb < NA; ++nb) w[nb] = tile_softmax<D, false>(st[nb], acc[nb], j0, pos[nb], P.c);
+    } else {
+#pragma unroll
+      for (int nb = 0; nb < NA; ++nb) w[nb] = tile_softmax<D, true>(st[nb], acc[nb], j0, pos[nb], P.c);
+    }
 #pragma unroll
     for (int m = 0; m < D / 16; ++m) {
       const u16x8 v0 = cat4(vh[m][0], vh[m][1]), v1 = cat4(vh[m][2], vh[m][3]);
@@ -576,20 +584,23 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   const int wave = uni(threadIdx.x >> 6);
   const int lane = __lane_id();
   const int col = lane & 15;
-  // Blocks of one XCD (block id mod 8) take a contiguous range of the items
-  // so that the q-tiles of one (request, KV head) share that XCD's L2.
-  const int total = P.off_chunk[P.num_seqs];
+  // Items are ordered (KV head, request, q-tile) and blocks of one XCD (block
+  // id mod 8) take a contiguous range of them: the q-tiles of one (request,
+  // KV head) share that XCD's L2, and with 8 KV heads each XCD takes one head
+  // of every request, so long and short requests spread over all XCDs.
+  const int per_head = P.off_chunk[P.num_seqs];
+  const int total = per_head * P.hkv;
   const int per_xcd = (total + 7) / 8;
   const int jx = (int)(blockIdx.x / 8);
   if (jx >= per_xcd) return;
   const int i = uni((int)(blockIdx.x % 8) * per_xcd + jx);
   if (i >= total) return;
-  const int r = find_req(P.off_chunk, P.num_seqs, i);
+  const int g = uni(i / per_head);
+  const int rem = i - g * per_head;
+  const int r = find_req(P.off_chunk, P.num_seqs, rem);
   const Req R = load_req(P, r);
   const int ncols = R.s * P.G;
-  const int qts = (ncols + kChunkCols - 1) / kChunkCols;
-  const int local = i - P.off_chunk[r];
-  const int g = uni(local / qts), qt = uni(local % qts);
+  const int qt = uni(rem - P.off_chunk[r]);
   const int c0 = qt * kChunkCols;
   const int cend = min(ncols, c0 + kChunkCols);
   const int pmax = R.n - R.s + (cend - 1) / P.G;  // last position of the block
@@ -698,8 +709,16 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
           [&](int b, int ks) { return *reinterpret_cast<const u16x8*>(T + b * BLK + 512 * ks + 8 * lane); },
           qf, acc);
       TileWeights w[NB];
+      bool open = true;  // every key of the tile visible to every column
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D>(st[nb], acc[nb], j0, pos[nb], P.c);
+      for (int nb = 0; nb < NB; ++nb) open = open && __all(pos[nb] >= j0 + kTileKeys - 1);
+      if (open) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D, false>(st[nb], acc[nb], j0, pos[nb], P.c);
+      } else {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D, true>(st[nb], acc[nb], j0, pos[nb], P.c);
+      }
 #pragma unroll
       for (int m = 0; m < D / 16; ++m) {
         const int o = 256 * m + 4 * lane;

@@ -59,11 +59,10 @@ __device__ __forceinline__ f32x4 mfma(const u16x8& a, const u16x8& b, const f32x
 // every kernel.  exp2(-inf) = 0 and exp2(+-0) = 1 exactly.
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// fp32 -> bf16 bits, round to nearest even (inputs here are finite).
+// fp32 -> bf16 bits, round to nearest even (v_cvt_pk_bf16_f32; the inputs
+// here are finite).
 __device__ __forceinline__ uint16_t bf16_rne(float f) {
-  uint32_t u = __builtin_bit_cast(uint32_t, f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 // Output cast: bf16 RNE, with -0 mapped to +0 (an all-zero row may carry
@@ -130,7 +129,11 @@ struct TileWeights {
   bool h;
 };
 
-template <int D>
+//
+// MASKED = false may be used only when every key of the tile is visible to
+// every column of the wavefront (p >= j0 + 63 in all lanes): all selects
+// then take their first operand, so both forms give the same bits.
+template <int D, bool MASKED = true>
 __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
                                                     const f32x4 (&acc)[kPagesPerTile], int j0,
                                                     int p, float c) {
@@ -142,7 +145,7 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int key = j0 + 16 * b + 4 * grp + i;
-      lam[b][i] = key <= p;
+      lam[b][i] = !MASKED || key <= p;
       g[b][i] = acc[b][i] * c;
     }
   // masked maximum over the tile: fixed tree in the lane, then lanes ^16, ^32
@@ -159,7 +162,7 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
   mx = fmax_(mx, xor_lane(mx, 16));
   mx = fmax_(mx, xor_lane(mx, 32));
   TileWeights w;
-  w.h = j0 <= p;  // any visible key in this tile for this column
+  w.h = !MASKED || j0 <= p;  // any visible key in this tile for this column
   w.m_new = fmax_(st.m, mx);
   // A column with no visible key keeps its state (tile_commit), and its
   // operands are zeroed so that nothing non-finite enters the matrix core.
