@@ -11,7 +11,8 @@ cfg + stream, *extra])))`` with streams
     0: lengths and offsets, 1: Q, 2: K, 3: V, 4: page placement A,
     5: page placement B, 6: the probe request, 7: companion requests.
 
-Values: iid N(0, 1) float32 rounded to bf16 with round-to-nearest-even.
+Values: iid N(0, 1) float32 (torch's CPU generator, seeded from the stream
+above) rounded to bf16 with round-to-nearest-even.
 Pools: pages are a random permutation of the pool; each request takes
 consecutive entries of it, so its pages are scattered.  Unused pages and
 slots at positions >= n hold a poison value (bf16 quiet NaN) unless told
@@ -72,7 +73,17 @@ def rng_for(cfg: int, stream: int, *extra: int) -> np.random.Generator:
 
 
 def normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
-    return bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    """iid N(0, 1) values rounded to bf16 (nearest even), as uint16 bits.
+
+    The values come from torch's CPU generator (deterministic for a given
+    seed whatever the thread count, and several times faster than numpy's
+    for the gigabyte-sized pools), seeded from ``rng``."""
+    import torch
+
+    g = torch.Generator().manual_seed(int(rng.integers(0, 2**63 - 1)))
+    n = int(np.prod(shape)) if len(shape) else 1
+    x = torch.randn(n, generator=g, dtype=torch.float32).to(torch.bfloat16)
+    return x.view(torch.int16).numpy().view(np.uint16).reshape(shape)
 
 
 # ---------------------------------------------------------------------------
@@ -200,6 +211,30 @@ class Call:
         assert r.n - r.s <= position < r.n
         return int(self.cu_q_lens[req_index]) + position - (r.n - r.s)
 
+    def subcall(self, req_indices: Sequence[int]) -> "Call":
+        """The same requests' logical data in a compact pool: only the pages
+        of the selected requests, renumbered in table order."""
+        P = self.shape.page_size
+        remap: Dict[int, int] = {}
+        owner: Dict[int, Tuple[int, int]] = {}
+        pt = np.full((len(req_indices), max(self.page_table.shape[1], 1)), -1, np.int32)
+        for k, i in enumerate(req_indices):
+            r = self.reqs[i]
+            for b in range(-(-r.n // P)):
+                pg = int(self.page_table[i, b])
+                if pg not in remap:
+                    remap[pg] = len(remap)
+                    # a page shared by several prompts holds the same data for
+                    # each of them: take it from this request's prompt
+                    owner[remap[pg]] = (r.prompt, b)
+                pt[k, b] = remap[pg]
+        return Call(self.shape, self.prompts, [self.reqs[i] for i in req_indices], pt,
+                    max(len(remap), 1), owner)
+
+    def request_of_row(self, row: int) -> int:
+        cu = self.cu_q_lens
+        return int(np.searchsorted(cu, row, side="right") - 1)
+
     # -- pool contents ------------------------------------------------------
     def kv_bytes(self) -> int:
         """Algorithmic K+V bytes: every request reads its n keys once."""
@@ -231,17 +266,35 @@ class Call:
         any request of this call that reads it."""
         return max(r.n for r in self.reqs if r.prompt == pid)
 
-    def std_pool(self, poison: bool = True) -> Tuple[np.ndarray, np.ndarray]:
-        """Pool in the plain layout [num_pages, Hkv, P, D] (uint16)."""
+    def std_pool(self, poison: bool = True, prompts=None) -> Tuple[np.ndarray, np.ndarray]:
+        """Pool in the plain layout [num_pages, Hkv, P, D] (uint16).  With
+        ``prompts`` (a set of prompt indices) only their pages are filled."""
         sh = self.shape
-        shape = (self.num_pages, sh.num_kv_heads, sh.page_size, sh.head_dim)
+        P = sh.page_size
+        shape = (self.num_pages, sh.num_kv_heads, P, sh.head_dim)
         fill = BF16_QNAN if poison else np.uint16(0)
         kp = np.full(shape, fill, np.uint16)
         vp = np.full(shape, fill, np.uint16)
-        k, v, slots = self.write_list()
-        pages, offs = slots // sh.page_size, slots % sh.page_size
-        kp[pages, :, offs, :] = k
-        vp[pages, :, offs, :] = v
+        by_prompt: Dict[int, List[Tuple[int, int]]] = {}
+        for page, (pid, lp) in self.page_owner.items():
+            if prompts is None or pid in prompts:
+                by_prompt.setdefault(pid, []).append((lp, page))
+        for pid, lst in by_prompt.items():
+            lst.sort()
+            pr = self.prompts[pid]
+            n = self.filled_len(pid)
+            lps = np.array([lp for lp, _ in lst])
+            pages = np.array([pg for _, pg in lst])
+            full = lps < n // P  # pages with all P slots filled
+            if full.any():
+                idx = lps[full][:, None] * P + np.arange(P)  # [pages, P] positions
+                kp[pages[full]] = pr.k[idx].transpose(0, 2, 1, 3)
+                vp[pages[full]] = pr.v[idx].transpose(0, 2, 1, 3)
+            for lp, page in zip(lps[~full], pages[~full]):
+                lo, hi = lp * P, min(lp * P + P, n)
+                if hi > lo:
+                    kp[page, :, :hi - lo, :] = pr.k[lo:hi].transpose(1, 0, 2)
+                    vp[page, :, :hi - lo, :] = pr.v[lo:hi].transpose(1, 0, 2)
         return kp, vp
 
 

@@ -78,11 +78,25 @@ def by_position(call: W.Call, out: np.ndarray):
 
 
 def parity(call: W.Call, gpu_bits: np.ndarray, rows=None) -> dict:
-    """Compares GPU rows with the oracle; returns error statistics."""
-    ref = oracle_run(call, rows)
+    """Compares GPU rows with the oracle; returns error statistics.
+
+    With ``rows``, the oracle runs on a compact copy of just the requests
+    holding those rows (their logical data and lengths are unchanged)."""
     got = W.bf16_to_f32(gpu_bits).astype(np.float64)
-    sel = np.arange(call.total_q_tokens) if rows is None else np.asarray(rows)
-    diff = np.abs(got[sel] - ref[sel])
+    if rows is None:
+        sel = np.arange(call.total_q_tokens)
+        ref = oracle_run(call)[sel]
+    else:
+        sel = np.asarray(rows)
+        reqs = sorted({call.request_of_row(int(t)) for t in sel})
+        sub = call.subcall(reqs)
+        sub_rows = []
+        for t in sel:
+            ri = call.request_of_row(int(t))
+            p = call.reqs[ri].n - call.reqs[ri].s + (int(t) - int(call.cu_q_lens[ri]))
+            sub_rows.append(sub.row_of(reqs.index(ri), p))
+        ref = oracle_run(sub, sub_rows)[sub_rows]
+    diff = np.abs(got[sel] - ref)
     assert np.isfinite(got[sel]).all(), "non-finite GPU output"
     st = dict(max_abs=float(diff.max()) if diff.size else 0.0,
               mean_abs=float(diff.mean()) if diff.size else 0.0, rows=int(len(sel)))

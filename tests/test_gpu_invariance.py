@@ -145,3 +145,19 @@ def test_long_context_batch_and_placement():
     b4 = outs(W.config4(batch=4, **kw))
     for i in range(4):
         U.assert_same_bits(b4, outs(W.config4(batch=4, only=i, perm_stream=5, **kw)))
+
+
+def test_full_size_long_decode_batch_one_vs_eight():
+    """Long-context decode at full size: requests alone (another placement)
+    and in the batch of 8 give the same bits."""
+    b8 = outs(W.config4())
+    for i in (2, 6):
+        U.assert_same_bits(b8, outs(W.config4(only=i, perm_stream=5)))
+
+
+def test_full_size_decode_probe_batch_1_17_64():
+    """Llama-3-8B decode at full size: the probe request alone, in 17 and in
+    64 requests (contexts 512..4096)."""
+    solo = outs(W.config2(batch=1, probe_slot=0))
+    for batch, slot in [(17, 9), (64, 33)]:
+        U.assert_same_bits(solo, outs(W.config2(batch=batch, probe_slot=slot, perm_stream=5)))

@@ -124,3 +124,44 @@ def test_parity_full_size_decode_sampled():
     out = U.gpu_run(call, poison=False)
     rows = np.random.default_rng(3).choice(call.total_q_tokens, 16, replace=False)
     U.say("  %s" % U.parity(call, out, rows=rows))
+
+
+def _sample_rows(call, per_req=2, max_reqs=6, seed=0):
+    """First and last query row of up to ``max_reqs`` requests, plus random rows."""
+    rng = np.random.default_rng(seed)
+    reqs = sorted(rng.choice(call.num_seqs, min(max_reqs, call.num_seqs), replace=False))
+    rows = set()
+    for ri in reqs:
+        lo, hi = int(call.cu_q_lens[ri]), int(call.cu_q_lens[ri + 1])
+        rows.update({lo, hi - 1})
+        rows.update(int(x) for x in rng.integers(lo, hi, size=per_req))
+    return sorted(rows)
+
+
+def test_parity_full_size_mixed_sampled():
+    """Mixed 8B batch at full size: 8 prefill chunks of 512 at offsets up to
+    8192 plus 120 decodes, in the benchmark's launch configuration."""
+    call = W.config3()
+    U.say("full cfg3: T=%d kv=%.2f GB" % (call.total_q_tokens, call.kv_bytes() / 1e9))
+    out = U.gpu_run(call, poison=False)
+    rows = _sample_rows(call, per_req=3, max_reqs=10)
+    rows += [int(call.cu_q_lens[i]) for i in range(8)]  # first row of every chunk
+    U.say("  %s" % U.parity(call, out, rows=sorted(set(rows))))
+
+
+def test_parity_full_size_long_decode_sampled():
+    """Long-context decode at full size (8 requests, contexts 32K..128K)."""
+    call = W.config4()
+    U.say("full cfg4: kv=%.2f GB max_n=%d" % (call.kv_bytes() / 1e9, call.max_context_len))
+    out = U.gpu_run(call, poison=False)
+    longest = int(np.argmax(call.context_lens))
+    U.say("  %s" % U.parity(call, out, rows=sorted({0, 5, longest})))
+
+
+def test_parity_full_size_verify_sampled():
+    """70B prefix-shared verify at full size (256 requests on a shared
+    2048-token prefix, s = 4 / 1)."""
+    call = W.config5()
+    U.say("full cfg5: T=%d kv(logical)=%.2f GB" % (call.total_q_tokens, call.kv_bytes() / 1e9))
+    out = U.gpu_run(call, poison=False)
+    U.say("  %s" % U.parity(call, out, rows=_sample_rows(call, per_req=2, max_reqs=8)))
