@@ -1,9 +1,9 @@
 """Benchmark of the paged-attention hot path on one MI355X.
 
 A step is one pass of the whole path over one batch: the KV-cache write of
-the batch's new tokens (vd_kv_write) followed by attention (the split, chunk
-and merge phases of vd_attn_forward), on synthetic bf16 inputs already
-resident in HBM.  R replicas of the inputs (pools, page tables, queries) are
+the batch's new tokens followed by attention, i.e. the plan phase (which also
+writes the new tokens into the pool), then the split, chunk and merge phases
+of vd_attn_forward, on synthetic bf16 inputs already resident in HBM.  R replicas of the inputs (pools, page tables, queries) are
 cycled so that no step finds its K/V in the 256 MB last-level cache left
 behind by the previous step.
 
@@ -160,18 +160,14 @@ def main():
         dc = S.to_device(attn, call, poison=False)
         ws = attn.new_workspace(call.num_seqs, dc.batch.max_q_len, dc.batch.max_context_len)
         reps.append((dc, ws, torch.empty_like(dc.batch.q)))
-    # this step's new tokens: positions n - s .. n - 1 of every request
     P = sh.page_size
-    kn, vn, slots = [], [], []
-    for ri, r in enumerate(call.reqs):
-        pr = call.prompts[r.prompt]
-        for p in r.positions:
-            kn.append(pr.k[p])
-            vn.append(pr.v[p])
-            slots.append(int(call.page_table[ri, p // P]) * P + p % P)
-    k_new = S.bf16_tensor(np.stack(kn), "cuda")
-    v_new = S.bf16_tensor(np.stack(vn), "cuda")
-    slot_t = torch.tensor(slots, dtype=torch.int64, device="cuda")
+    # this step's new tokens (positions n - s .. n - 1 of every request): the
+    # plan phase writes them into the pool before attention reads it
+    kn, vn, sl = call.new_tokens()
+    k_new, v_new = S.bf16_tensor(kn, "cuda"), S.bf16_tensor(vn, "cuda")
+    slot_t = torch.from_numpy(sl).cuda()
+    for dc, _, _ in reps:
+        dc.batch.k_new, dc.batch.v_new, dc.batch.slot_mapping = k_new, v_new, slot_t
     torch.cuda.synchronize()
     log("staged %d replicas" % len(reps))
 
@@ -189,14 +185,12 @@ def main():
         dc, ws, out = reps[i % len(reps)]
         b = dc.batch
         phases = [
-            lambda: attn.kv_write(k_new, v_new, slot_t, b.k_pool, b.v_pool, b.num_pages,
-                                  stream=stream),
             lambda: attn.forward_plan(b, ws, stream=stream),
             lambda: attn.forward_splits(b, out, ws, stream=stream),
             lambda: attn.forward_chunks(b, out, ws, stream=stream),
             lambda: attn.forward_merge(b, out, ws, stream=stream),
         ]
-        names = ["kv_write", "plan", "splits", "chunks", "merge"]
+        names = ["plan_and_kv_write", "splits", "chunks", "merge"]
         for j, (name, fn) in enumerate(zip(names, phases)):
             if all_ev is not None:
                 all_ev[j].record(stream)
@@ -208,14 +202,6 @@ def main():
         if all_ev is not None:
             all_ev[len(phases)].record(stream)
 
-    if args.copy_calibration_mb:
-        n = (args.copy_calibration_mb << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        torch.neg(src, out=dst)
-        torch.cuda.synchronize()
-        del src, dst
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -229,13 +215,13 @@ def main():
     ms = elapsed * 1e3 / args.steps
     dom_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     # diagnostic pass (not the timed region): every phase bracketed
-    diag = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(10)]
+    diag = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(10)]
     for i in range(10):
         step(i, all_ev=diag[i])
     torch.cuda.synchronize()
-    ph_ms = np.mean([[e[j].elapsed_time(e[j + 1]) for j in range(5)] for e in diag], axis=0)
-    log("timed: %.4f ms/step, %s kernel %.4f ms; diagnostic phases (ms): kv_write %.4f "
-        "plan %.4f splits %.4f chunks %.4f merge %.4f" % (ms, dominant, dom_ms, *ph_ms))
+    ph_ms = np.mean([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in diag], axis=0)
+    log("timed: %.4f ms/step, %s kernel %.4f ms; diagnostic phases (ms): plan+kv_write %.4f "
+        "splits %.4f chunks %.4f merge %.4f" % (ms, dominant, dom_ms, *ph_ms))
 
     kv_bytes = call.kv_bytes()
     T = call.total_q_tokens
@@ -275,7 +261,7 @@ def main():
         "hbm_frac_whole_step": round(value / HBM_PEAK_GBS, 4),
         "tokens_per_s": round(T / (ms * 1e-3), 1),
         "phase_ms_diagnostic": {k: round(float(v), 5) for k, v in
-                                zip(["kv_write", "plan", "splits", "chunks", "merge"], ph_ms)},
+                                zip(["plan_and_kv_write", "splits", "chunks", "merge"], ph_ms)},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

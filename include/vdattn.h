@@ -107,6 +107,13 @@ typedef struct {
   int64_t num_pages;            /* >= 1 */
   int32_t max_q_len;            /* HOST hint: >= every s_r (launch sizing only) */
   int32_t max_context_len;      /* HOST hint: >= every n_r (launch sizing only) */
+  /* Optional: this call's new tokens, written into the pool by the plan phase
+   * before any attention kernel reads it (append + attend in one call; the
+   * same arguments and layout as vd_kv_write).  k_new == NULL: none. */
+  const void* k_new;            /* [num_new_tokens, Hkv, D] bf16 */
+  const void* v_new;            /* [num_new_tokens, Hkv, D] bf16 */
+  const int64_t* slot_mapping;  /* [num_new_tokens], slot = page * 16 + offset; < 0 skips */
+  int64_t num_new_tokens;       /* >= 0 */
 } vd_attn_batch;
 
 /* Bytes of workspace one call needs for the given host-side sizes: the plan
@@ -127,9 +134,10 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, voi
 /* The four phases vd_attn_forward runs, in this order, for callers that time
  * or schedule them separately (same batch, same output, same stream, same
  * workspace; their composition is bit-identical to vd_attn_forward):
- *   plan:   reads the per-request lengths on the device and writes the
- *           compact work lists of the split and chunk phases into the
- *           workspace (no device-to-host synchronisation);
+ *   plan:   writes the batch's new tokens into the pool (when given) and,
+ *           reading the per-request lengths on the device, the compact work
+ *           lists of the split and chunk phases into the workspace (no
+ *           device-to-host synchronisation);
  *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
  *           per (request, KV head, 512-key split).  A request with one split
  *           writes its output rows directly; otherwise each item writes a

@@ -5,7 +5,7 @@
 //                 prefix offsets of three compact work lists into the
 //                 workspace, so that no launched wavefront is idle in the
 //                 middle of the grid (no device-to-host synchronisation).
-//   split kernel  one wavefront per (request, KV head, 512-key split) for
+//   split kernel  one wavefront (workgroup) per (request, KV head, 512-key split) for
 //                 requests with at most 32 query-head rows per KV head
 //                 (decode, verify).  K/V go straight from HBM to registers
 //                 in the matrix-core operand layout; writes a partial state.
@@ -52,6 +52,11 @@ struct Params {
   int num_seqs, pt_stride, max_q, max_ctx, max_splits, split_cols;
   int hq, hkv, G;
   float c;  // softmax scale * log2(e), rounded once to fp32 on the host
+  // optional new tokens written by the plan launch
+  const uint16_t* knew;
+  const uint16_t* vnew;
+  const int64_t* slots;
+  int64_t num_new;
 };
 
 struct Req {
@@ -153,8 +158,39 @@ __device__ __forceinline__ void store_row(const Params& P, const f32x4 (&u)[D / 
   }
 }
 
+// Writes one (token, KV head, 8 consecutive d) of new K/V into the pools.
+template <int D>
+__device__ __forceinline__ void kv_write_one(const uint16_t* knew, const uint16_t* vnew,
+                                             const int64_t* slots, int64_t ntok, uint16_t* kpool,
+                                             uint16_t* vpool, int64_t num_pages, int hkv,
+                                             int64_t id) {
+  const int64_t per_tok = (int64_t)hkv * (D / 8);
+  if (id >= ntok * per_tok) return;
+  const int64_t t = id / per_tok;
+  const int hd = (int)(id % per_tok);
+  const int h = hd / (D / 8);
+  const int dc = hd % (D / 8);
+  const int64_t slot = slots[t];
+  if (slot < 0 || slot >= num_pages * kPage) return;
+  const int64_t page = slot / kPage;
+  const int s = (int)(slot % kPage);
+  const int64_t blk = (page * hkv + h) * (int64_t)(kPage * D);
+  const int64_t src = (t * hkv + h) * D + 8 * dc;
+  const u16x8 kv = *reinterpret_cast<const u16x8*>(knew + src);
+  const u16x8 vv = *reinterpret_cast<const u16x8*>(vnew + src);
+  // K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
+  *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + s) * 8) = kv;
+  // V block: element (slot, d) at ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int d = 8 * dc + e;
+    vpool[blk + ((d / 16) * 4 + s / 4) * 64 + (d % 16) * 4 + s % 4] = vv[e];
+  }
+}
+
 // ---------------------------------------------------------------------------
-// plan kernel: one workgroup of 1024 threads
+// plan kernel: workgroup 0 (1024 threads) plans; workgroups 1.. write the
+// call's new tokens into the pool
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int wave_incl_scan(int v) {
   const int lane = __lane_id();
@@ -166,7 +202,15 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
+template <int D>
 __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
+  if (blockIdx.x > 0) {
+    // the new tokens of the call (workgroups 1..)
+    kv_write_one<D>(P.knew, P.vnew, P.slots, P.num_new, const_cast<uint16_t*>(P.kpool),
+                    const_cast<uint16_t*>(P.vpool), P.num_pages, P.hkv,
+                    (int64_t)(blockIdx.x - 1) * blockDim.x + threadIdx.x);
+    return;
+  }
   __shared__ int wsum[3][16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int base[3] = {0, 0, 0};
@@ -370,10 +414,11 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
   }
 }
 
+// One wavefront per workgroup: a finished item frees its slot at once, which
+// keeps the end of the launch short when item durations vary.
 template <int D, int NB>
-__global__ __launch_bounds__(256) void split_kernel(Params P) {
-  const int wave = uni(threadIdx.x >> 6);
-  const int i = uni(blockIdx.x * 4 + wave);
+__global__ __launch_bounds__(64) void split_kernel(Params P) {
+  const int i = uni(blockIdx.x);
   const int tot_full = P.off_full[P.num_seqs], tot_part = P.off_part[P.num_seqs];
   int r, g, k;
   Req R;
@@ -400,6 +445,9 @@ __global__ __launch_bounds__(256) void split_kernel(Params P) {
     split_item<D, 1>(P, r, g, k, R);
 }
 
+// Contexts of up to this many splits are merged by the short merge kernel.
+constexpr int kShortMerge = 16;
+
 // ---------------------------------------------------------------------------
 // short merge (contexts of at most 16 splits): one thread per (request, KV
 // head, column, 4 consecutive d), folding the partial states in ascending
@@ -422,15 +470,29 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   const int MS = P.max_splits;
   const int kp = (R.n - R.s + c / P.G) / kSplitKeys + 1;
   const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS;
-  float M = P.ws_m[p0], Z = P.ws_z[p0];
-  f32x4 W = *reinterpret_cast<const f32x4*>(P.ws_u + p0 * D + d);
-  for (int k = 1; k < kp; ++k) {
-    const FoldScalars f = fold_scalars(M, Z, P.ws_m[p0 + k], P.ws_z[p0 + k]);
-    const f32x4 uk = *reinterpret_cast<const f32x4*>(P.ws_u + (p0 + k) * D + d);
+  // every partial state is loaded first (at most kShortMerge of them), then
+  // folded in ascending split order
+  float mk[kShortMerge], zk[kShortMerge];
+  f32x4 uk[kShortMerge];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) W[i] = fold_value(W[i], uk[i], f);
-    M = f.M;
-    Z = f.Z;
+  for (int k = 0; k < kShortMerge; ++k) {
+    if (k < kp) {
+      mk[k] = P.ws_m[p0 + k];
+      zk[k] = P.ws_z[p0 + k];
+      uk[k] = *reinterpret_cast<const f32x4*>(P.ws_u + (p0 + k) * D + d);
+    }
+  }
+  float M = mk[0], Z = zk[0];
+  f32x4 W = uk[0];
+#pragma unroll
+  for (int k = 1; k < kShortMerge; ++k) {
+    if (k < kp) {
+      const FoldScalars f = fold_scalars(M, Z, mk[k], zk[k]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) W[i] = fold_value(W[i], uk[k][i], f);
+      M = f.M;
+      Z = f.Z;
+    }
   }
   const float rho = final_scale(Z);
   u16x4 o;
@@ -771,35 +833,13 @@ constexpr size_t chunk_lds_bytes() {
 
 // ---------------------------------------------------------------------------
 // KV write: one thread per (token, KV head, 8 consecutive d)
-// ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void kv_write_kernel(const uint16_t* knew, const uint16_t* vnew,
                                                        const int64_t* slots, int64_t ntok,
                                                        uint16_t* kpool, uint16_t* vpool,
                                                        int64_t num_pages, int hkv) {
-  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t per_tok = (int64_t)hkv * (D / 8);
-  if (id >= ntok * per_tok) return;
-  const int64_t t = id / per_tok;
-  const int hd = (int)(id % per_tok);
-  const int h = hd / (D / 8);
-  const int dc = hd % (D / 8);
-  const int64_t slot = slots[t];
-  if (slot < 0 || slot >= num_pages * kPage) return;
-  const int64_t page = slot / kPage;
-  const int s = (int)(slot % kPage);
-  const int64_t blk = (page * hkv + h) * (int64_t)(kPage * D);
-  const int64_t src = (t * hkv + h) * D + 8 * dc;
-  const u16x8 kv = *reinterpret_cast<const u16x8*>(knew + src);
-  const u16x8 vv = *reinterpret_cast<const u16x8*>(vnew + src);
-  // K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
-  *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + s) * 8) = kv;
-  // V block: element (slot, d) at ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int d = 8 * dc + e;
-    vpool[blk + ((d / 16) * 4 + s / 4) * 64 + (d % 16) * 4 + s % 4] = vv[e];
-  }
+  kv_write_one<D>(knew, vnew, slots, ntok, kpool, vpool, num_pages, hkv,
+                  (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
 }
 
 }  // namespace
@@ -885,6 +925,11 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.hkv = h->hkv;
   P.G = h->group;
   P.c = h->c;
+  const bool writes = b->k_new && b->num_new_tokens > 0;
+  P.knew = writes ? static_cast<const uint16_t*>(b->k_new) : nullptr;
+  P.vnew = writes ? static_cast<const uint16_t*>(b->v_new) : nullptr;
+  P.slots = writes ? b->slot_mapping : nullptr;
+  P.num_new = writes ? b->num_new_tokens : 0;
   return P;
 }
 
@@ -892,8 +937,12 @@ int launched() { return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH;
 
 
 
+template <int D>
 int run_plan(const Params& P, hipStream_t s) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, P);
+  const int64_t wthreads = P.knew ? P.num_new * P.hkv * (D / 8) : 0;
+  const int64_t blocks = 1 + (wthreads + 1023) / 1024;
+  if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
+  hipLaunchKernelGGL((plan_kernel<D>), dim3((unsigned)blocks), dim3(1024), 0, s, P);
   return launched();
 }
 
@@ -902,7 +951,7 @@ int run_splits(const Params& P, hipStream_t s) {
   // upper bound of the split items; items past the planned total exit at once
   const int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
   if (items > INT32_MAX - 4) return VD_ERR_INVALID_ARG;
-  const dim3 grid((unsigned)((items + 3) / 4)), block(256);
+  const dim3 grid((unsigned)items), block(64);
   if (P.split_cols == 16)
     hipLaunchKernelGGL((split_kernel<D, 1>), grid, block, 0, s, P);
   else
@@ -910,14 +959,10 @@ int run_splits(const Params& P, hipStream_t s) {
   return launched();
 }
 
-// Up to this many splits per request the short merge (one thread per output
-// quad, sequential fold) is used; beyond it the chunked merge kernel.
-constexpr int kShortMergeSplits = 16;
-
 template <int D>
 int run_merge(const Params& P, hipStream_t s) {
   const int64_t cols = std::min<int64_t>((int64_t)P.max_q * P.G, P.split_cols);
-  if (P.max_splits <= kShortMergeSplits) {
+  if (P.max_splits <= kShortMerge) {
     const int64_t threads = (int64_t)P.num_seqs * P.hkv * cols * (D / 4);
     const int64_t blocks = (threads + 255) / 256;
     if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
@@ -1003,7 +1048,11 @@ int vd_attn_forward_plan(const vd_attn* h, const vd_attn_batch* b, void* workspa
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
-  return run_plan(make_params(h, b, nullptr, workspace), stream);
+  if (b->num_new_tokens < 0 || (b->num_new_tokens > 0 && b->k_new &&
+                                 (!b->v_new || !b->slot_mapping)))
+    return VD_ERR_INVALID_ARG;
+  const Params P = make_params(h, b, nullptr, workspace);
+  return h->d == 64 ? run_plan<64>(P, stream) : run_plan<128>(P, stream);
 }
 
 int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* out, void* workspace,

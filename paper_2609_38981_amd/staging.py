@@ -39,9 +39,10 @@ def handle_for(shape: W.Shape) -> VdAttn:
 
 
 def fill_pool(attn: VdAttn, call: W.Call, k_pool: torch.Tensor, v_pool: torch.Tensor,
-              chunk_tokens: int = 1 << 16):
-    """Writes every valid slot of ``call`` into the pools with vd_kv_write."""
-    k, v, slots = call.write_list()
+              chunk_tokens: int = 1 << 16, exclude_new: bool = False):
+    """Writes every valid slot of ``call`` into the pools with vd_kv_write
+    (without this call's own tokens when ``exclude_new``)."""
+    k, v, slots = call.write_list(exclude_new=exclude_new)
     dev = k_pool.device
     for lo in range(0, slots.shape[0], chunk_tokens):
         hi = min(lo + chunk_tokens, slots.shape[0])
@@ -50,16 +51,23 @@ def fill_pool(attn: VdAttn, call: W.Call, k_pool: torch.Tensor, v_pool: torch.Te
 
 
 def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
-              hint_extra_q: int = 0, hint_extra_ctx: int = 0) -> DeviceCall:
+              hint_extra_q: int = 0, hint_extra_ctx: int = 0, append: bool = False) -> DeviceCall:
     """Device copy of ``call``.  Pools start as bf16 NaN (``poison``) or zero,
     then receive every valid slot; host hints are the call's true maxima plus
-    the given extras."""
+    the given extras.  With ``append``, this call's own tokens are not written
+    to the pool but handed to the batch (k_new, v_new, slot_mapping), for the
+    library to write before attention."""
     fill = int(np.int16(np.uint16(W.BF16_QNAN).view(np.int16))) if poison else 0
     k_pool = attn.new_pool(call.num_pages, device)
     v_pool = attn.new_pool(call.num_pages, device)
     k_pool.view(torch.int16).fill_(fill)
     v_pool.view(torch.int16).fill_(fill)
-    fill_pool(attn, call, k_pool, v_pool)
+    fill_pool(attn, call, k_pool, v_pool, exclude_new=append)
+    extra = {}
+    if append:
+        kn, vn, sl = call.new_tokens()
+        extra = dict(k_new=bf16_tensor(kn, device), v_new=bf16_tensor(vn, device),
+                     slot_mapping=torch.from_numpy(sl).to(device))
     batch = Batch(
         q=bf16_tensor(call.q_bits(), device),
         cu_q_lens=torch.from_numpy(call.cu_q_lens).to(device),
@@ -67,5 +75,5 @@ def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
         page_table=torch.from_numpy(np.ascontiguousarray(call.page_table)).to(device),
         k_pool=k_pool, v_pool=v_pool, num_pages=call.num_pages,
         max_q_len=max(call.max_q_len, 1) + hint_extra_q,
-        max_context_len=max(call.max_context_len, 1) + hint_extra_ctx)
+        max_context_len=max(call.max_context_len, 1) + hint_extra_ctx, **extra)
     return DeviceCall(call, batch)

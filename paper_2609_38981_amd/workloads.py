@@ -241,9 +241,31 @@ class Call:
         sh = self.shape
         return int(sum(r.n for r in self.reqs)) * sh.num_kv_heads * sh.head_dim * 2 * 2
 
-    def write_list(self) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    def new_tokens(self) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+        """This call's own tokens (positions n - s .. n - 1 of every request):
+        (k_rows, v_rows [N, Hkv, D] uint16, slot ids int64 [N])."""
+        P = self.shape.page_size
+        ks, vs, slots, seen = [], [], [], set()
+        for ri, r in enumerate(self.reqs):
+            pr = self.prompts[r.prompt]
+            for p in r.positions:
+                sl = int(self.page_table[ri, p // P]) * P + p % P
+                if sl in seen:
+                    continue
+                seen.add(sl)
+                ks.append(pr.k[p])
+                vs.append(pr.v[p])
+                slots.append(sl)
+        sh = self.shape
+        if not ks:
+            e = np.zeros((0, sh.num_kv_heads, sh.head_dim), np.uint16)
+            return e, e.copy(), np.zeros(0, np.int64)
+        return np.stack(ks), np.stack(vs), np.array(slots, np.int64)
+
+    def write_list(self, exclude_new: bool = False) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
         """Every valid physical slot once: (k_rows, v_rows [W, Hkv, D] uint16,
-        slot ids int64 [W] with slot = page * P + offset)."""
+        slot ids int64 [W] with slot = page * P + offset).  With
+        ``exclude_new``, the slots of this call's own tokens are left out."""
         P = self.shape.page_size
         ks, vs, slots = [], [], []
         for page, (pid, lp) in sorted(self.page_owner.items()):
@@ -259,7 +281,11 @@ class Call:
         if not ks:
             e = np.zeros((0, sh.num_kv_heads, sh.head_dim), np.uint16)
             return e, e.copy(), np.zeros(0, np.int64)
-        return np.concatenate(ks), np.concatenate(vs), np.concatenate(slots)
+        k, v, sl = np.concatenate(ks), np.concatenate(vs), np.concatenate(slots)
+        if exclude_new:
+            keep = ~np.isin(sl, self.new_tokens()[2])
+            k, v, sl = k[keep], v[keep], sl[keep]
+        return k, v, sl
 
     def filled_len(self, pid: int) -> int:
         """Positions of prompt ``pid`` present in the pool: the longest n of

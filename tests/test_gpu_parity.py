@@ -165,3 +165,15 @@ def test_parity_full_size_verify_sampled():
     U.say("full cfg5: T=%d kv(logical)=%.2f GB" % (call.total_q_tokens, call.kv_bytes() / 1e9))
     out = U.gpu_run(call, poison=False)
     U.say("  %s" % U.parity(call, out, rows=_sample_rows(call, per_req=2, max_reqs=8)))
+
+
+@pytest.mark.parametrize("name", ["cfg1_tiny", "cfg3_mixed_small", "cfg5_verify_small"])
+def test_append_then_attend(name):
+    """The call's own tokens handed to vd_attn_forward (written by its plan
+    phase) instead of written beforehand with vd_kv_write: the same bits, and
+    within tolerance of the oracle."""
+    call = SMALL[name]()
+    a = U.gpu_run(call, append=True)
+    b = U.gpu_run(call)
+    assert np.array_equal(a, b)
+    U.say("  append %s: %s" % (name, U.parity(call, a)))
