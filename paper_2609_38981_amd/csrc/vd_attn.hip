@@ -602,6 +602,13 @@ __global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
 // wavefronts compute tile t, the loads of tiles t + 1 and t + 2 are in
 // flight.  The splits are folded in registers as each one ends.
 // ---------------------------------------------------------------------------
+// Depth of the chunk kernel's LDS ring: tiles t + 1 .. t + kChunkStages - 1 are
+// in flight while tile t is computed.
+#ifndef VD_CHUNK_STAGES
+#define VD_CHUNK_STAGES 3
+#endif
+constexpr int kChunkStages = VD_CHUNK_STAGES;
+
 // Direct global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
 // byte address m0val + 16 l.  Issued as inline assembly so that the compiler
 // does not make every later LDS read wait for all such copies; the kernel
@@ -641,7 +648,7 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   constexpr int NBLK = 2 * kPagesPerTile;          // 4 K blocks then 4 V blocks
   constexpr int TILE = NBLK * BLK;                 // elements of one staged tile
   constexpr int WCH = TILE / (4 * 512);            // 1 KB copies per wavefront per tile
-  constexpr int STAGES = 3;
+  constexpr int STAGES = kChunkStages;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];  // [STAGES][NBLK][BLK]
   const int wave = uni(threadIdx.x >> 6);
   const int lane = __lane_id();
@@ -743,14 +750,21 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   };
 
   wait_vmcnt<0>();  // the Q operands are in registers before any tile copy is issued
-  fetch(0, 0);
-  if (ntiles > 1) fetch(1, 1);
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < ntiles) fetch(t, t);
   for (int kt = 0; kt < ntiles; ++kt) {
     const int j0 = kt * kTileKeys;
     const int k = kt / kTilesPerSplit;
     const int buf = kt % STAGES;
-    // tile kt has landed once at most the next tile's loads are outstanding
-    if (kt + 1 < ntiles)
+    // tile kt has landed once at most the later tiles' loads are outstanding
+    const int later = min(STAGES - 2, ntiles - 1 - kt);
+    static_assert(STAGES >= 2 && STAGES <= 5, "ring depth");
+    if (later >= 3)
+      wait_vmcnt<3 * WCH>();
+    else if (later == 2)
+      wait_vmcnt<2 * WCH>();
+    else if (later == 1)
       wait_vmcnt<WCH>();
     else
       wait_vmcnt<0>();
@@ -759,7 +773,7 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
       mask_stage(kt, buf);
       lds_barrier();
     }
-    if (kt + 2 < ntiles) fetch(kt + 2, (kt + 2) % STAGES);
+    if (kt + STAGES - 1 < ntiles) fetch(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     if (kt % kTilesPerSplit == 0) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) state_init(st[nb]);
@@ -825,10 +839,10 @@ __global__ __launch_bounds__(256) void chunk_kernel(Params P) {
   }
 }
 
-// Dynamic LDS bytes of the chunk kernel: 3 stages of 8 page blocks.
+// Dynamic LDS bytes of the chunk kernel: kChunkStages stages of 8 page blocks.
 template <int D>
 constexpr size_t chunk_lds_bytes() {
-  return (size_t)3 * 2 * kPagesPerTile * kPage * D * sizeof(uint16_t);
+  return (size_t)kChunkStages * 2 * kPagesPerTile * kPage * D * sizeof(uint16_t);
 }
 
 // ---------------------------------------------------------------------------
