@@ -2,15 +2,18 @@
 //
 // Kernels of one attention call, all on the caller's stream:
 //   plan kernel   one workgroup; reads the per-request lengths and writes
-//                 prefix offsets of three compact work lists into the
-//                 workspace, so that no launched wavefront is idle in the
-//                 middle of the grid (no device-to-host synchronisation).
+//                 prefix offsets of the compact work lists, and the split
+//                 work list itself, into the workspace, so that no launched
+//                 wavefront is idle in the middle of the grid (no
+//                 device-to-host synchronisation).  Its other workgroups
+//                 write the call's new tokens into the pool.
 //   split kernel  one wavefront (workgroup) per (request, KV head, 512-key split) for
 //                 requests with at most 32 query-head rows per KV head
 //                 (decode, verify).  K/V go straight from HBM to registers
 //                 in the matrix-core operand layout; writes a partial state.
 //                 Whole 512-key splits are listed before the shorter last
-//                 splits, so short items fill the end of the launch.
+//                 splits, and those by decreasing length, so the shortest
+//                 items fill the end of the launch.
 //   chunk kernel  one workgroup (4 wavefronts x 32 columns) per (request,
 //                 KV head, 128 query-head rows) for longer chunks (prefill);
 //                 K/V tiles are staged in LDS and shared by the wavefronts;
@@ -44,6 +47,7 @@ struct Params {
   int32_t* off_full;   // [num_seqs + 1] prefix offsets of whole-split items
   int32_t* off_part;   // [num_seqs + 1] prefix offsets of last-split items
   int32_t* off_chunk;  // [num_seqs + 1] prefix offsets of q-tiles (per KV head)
+  int32_t* items;      // [num_seqs * Hkv * max_splits][8] split work list
   float* ws_m;
   float* ws_z;
   float* ws_u;
@@ -202,6 +206,21 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
+// Work-list entry of one split item: request, KV head, split index and the
+// request's lengths, so that a split wavefront reaches its first K/V loads
+// after a single scalar load.  r = -1 marks an unused grid slot.
+constexpr int kItemInts = 8;  // {r, g, k, n, q0, s, 0, 0}
+// Number of counters of the planning scan: whole splits, chunk q-tiles, and
+// the last (partial) splits by their tile count, 8 down to 1.
+constexpr int kPlanCounters = 2 + kTilesPerSplit;
+
+__device__ __forceinline__ void put_item(const Params& P, int64_t idx, int r, int g, int k,
+                                         const Req& R) {
+  int4* e = reinterpret_cast<int4*>(P.items + idx * kItemInts);
+  e[0] = int4{r, g, k, R.n};
+  e[1] = int4{R.q0, R.s, 0, 0};
+}
+
 template <int D>
 __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
   if (blockIdx.x > 0) {
@@ -211,53 +230,117 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
                     (int64_t)(blockIdx.x - 1) * blockDim.x + threadIdx.x);
     return;
   }
-  __shared__ int wsum[3][16];
+  constexpr int NC = kPlanCounters;
+  __shared__ int wsum[NC][16];  // per-wavefront totals of each counter
+  __shared__ int wpre[NC][16];  // offset of each (counter, wavefront)
+  __shared__ int sbase[NC];     // running totals over the request chunks
+  __shared__ int pstart[NC];    // first item of each partial-split class
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int base[3] = {0, 0, 0};
+  const unsigned long long below = (1ull << lane) - 1;
+  if (tid < NC) sbase[tid] = 0;
+  __syncthreads();
+  // Pass 1: prefix offsets.  Split items: every whole split, then the last
+  // partial splits ordered by decreasing tile count (longest first), so that
+  // the items that start late in the launch are the shortest.  Counter 0:
+  // whole-split items; 1: chunk q-tiles per KV head; 2 + 8 - t: requests whose
+  // last split has t tiles (Hkv items each), counted with ballots.
   for (int r0 = 0; r0 < P.num_seqs; r0 += 1024) {
     const int r = r0 + tid;
-    int cnt[3] = {0, 0, 0};
+    int cfull = 0, cchunk = 0, cls = -1;
     if (r < P.num_seqs) {
       const Req R = load_req(P, r);
       if (R.valid) {
         const int ncols = R.s * P.G;
         if (ncols <= P.split_cols) {
-          cnt[0] = P.hkv * (R.n / kSplitKeys);
-          cnt[1] = (R.n % kSplitKeys) ? P.hkv : 0;
+          cfull = P.hkv * (R.n / kSplitKeys);
+          const int rest = R.n % kSplitKeys;
+          if (rest) cls = 2 + kTilesPerSplit - (rest + kTileKeys - 1) / kTileKeys;
         } else if (ncols > kSplitCols) {
-          cnt[2] = (ncols + kChunkCols - 1) / kChunkCols;  // q-tiles per KV head
+          cchunk = (ncols + kChunkCols - 1) / kChunkCols;  // q-tiles per KV head
         }
       }
     }
-    int incl[3];
+    const int ifull = wave_incl_scan(cfull), ichunk = wave_incl_scan(cchunk);
+    int rank = 0;  // requests of the same class below this lane in the wavefront
 #pragma unroll
-    for (int a = 0; a < 3; ++a) {
-      incl[a] = wave_incl_scan(cnt[a]);
-      if (lane == 63) wsum[a][wave] = incl[a];
+    for (int c = 2; c < NC; ++c) {
+      const unsigned long long m = __ballot(cls == c);
+      rank = cls == c ? __popcll(m & below) : rank;
+      if (lane == 0) wsum[c][wave] = __popcll(m) * P.hkv;
+    }
+    if (lane == 63) {
+      wsum[0][wave] = ifull;
+      wsum[1][wave] = ichunk;
     }
     __syncthreads();
-    int pre[3] = {0, 0, 0}, tot[3] = {0, 0, 0};
-#pragma unroll
-    for (int a = 0; a < 3; ++a)
-      for (int w = 0; w < 16; ++w) {
-        const int v = wsum[a][w];
-        pre[a] += w < wave ? v : 0;
-        tot[a] += v;
-      }
-    if (r < P.num_seqs) {
-      P.off_full[r] = base[0] + pre[0] + incl[0] - cnt[0];
-      P.off_part[r] = base[1] + pre[1] + incl[1] - cnt[1];
-      P.off_chunk[r] = base[2] + pre[2] + incl[2] - cnt[2];
+    if (tid < NC * 16) {
+      const int c = tid / 16, w = tid % 16;
+      int pre = sbase[c];
+      for (int x = 0; x < w; ++x) pre += wsum[c][x];
+      wpre[c][w] = pre;
     }
-#pragma unroll
-    for (int a = 0; a < 3; ++a) base[a] += tot[a];
+    __syncthreads();
+    if (r < P.num_seqs) {
+      P.off_full[r] = wpre[0][wave] + ifull - cfull;
+      P.off_part[r] = cls >= 2 ? wpre[cls][wave] + rank * P.hkv : 0;  // within its class
+      P.off_chunk[r] = wpre[1][wave] + ichunk - cchunk;
+    }
+    if (tid < NC) sbase[tid] = wpre[tid][15] + wsum[tid][15];
     __syncthreads();
   }
   if (tid == 0) {
-    P.off_full[P.num_seqs] = base[0];
-    P.off_part[P.num_seqs] = base[1];
-    P.off_chunk[P.num_seqs] = base[2];
+    int t = sbase[0];
+    for (int c = 2; c < NC; ++c) {
+      pstart[c] = t;
+      t += sbase[c];
+    }
+    pstart[0] = t;  // total number of split items
+    P.off_full[P.num_seqs] = sbase[0];
+    P.off_part[P.num_seqs] = t - sbase[0];
+    P.off_chunk[P.num_seqs] = sbase[1];
   }
+  __syncthreads();
+  const int total = pstart[0];
+  // Pass 2: the split work list.  Wavefront w lists the items of requests
+  // w, w + 16, ...: lane j first reads the lengths and offsets of request
+  // w + 16 j, then the wavefront takes the requests in turn, its lanes
+  // writing one entry each.  Whole splits of a request are listed
+  // KV-head-major: item off_full + g * nfull + k.
+  for (int rb = 0; rb < P.num_seqs; rb += 1024) {
+    const int rl = rb + wave + 16 * lane;
+    int q0 = 0, s = 0, n = 0, fo = 0, po = -1;  // po < 0: no split items
+    if (rl < P.num_seqs) {
+      const Req R = load_req(P, rl);
+      if (R.valid && R.s * P.G <= P.split_cols) {
+        q0 = R.q0;
+        s = R.s;
+        n = R.n;
+        fo = P.off_full[rl];
+        const int rest = R.n % kSplitKeys;
+        po = rest ? pstart[2 + kTilesPerSplit - (rest + kTileKeys - 1) / kTileKeys] + P.off_part[rl]
+                  : 0;
+      }
+    }
+    for (int j = 0; j < 64; ++j) {
+      const int r = rb + wave + 16 * j;
+      if (r >= P.num_seqs) break;
+      if (__builtin_amdgcn_readlane(po, j) < 0) continue;
+      Req R;
+      R.q0 = __builtin_amdgcn_readlane(q0, j);
+      R.s = __builtin_amdgcn_readlane(s, j);
+      R.n = __builtin_amdgcn_readlane(n, j);
+      R.valid = true;
+      const int rfo = __builtin_amdgcn_readlane(fo, j), rpo = __builtin_amdgcn_readlane(po, j);
+      const int nfull = R.n / kSplitKeys;
+      for (int idx = lane; idx < P.hkv * nfull; idx += 64)
+        put_item(P, (int64_t)rfo + idx, r, idx / nfull, idx % nfull, R);
+      if (R.n % kSplitKeys)
+        for (int g = lane; g < P.hkv; g += 64) put_item(P, (int64_t)rpo + g, r, g, nfull, R);
+    }
+  }
+  // Pass 3: grid slots past the list exit at once
+  const int64_t upper = (int64_t)P.num_seqs * P.hkv * P.max_splits;
+  for (int64_t i = total + tid; i < upper; i += 1024) P.items[i * kItemInts] = -1;
 }
 
 // ---------------------------------------------------------------------------
@@ -418,26 +501,22 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 // keeps the end of the launch short when item durations vary.
 template <int D, int NB>
 __global__ __launch_bounds__(64) void split_kernel(Params P) {
-  const int i = uni(blockIdx.x);
-  const int tot_full = P.off_full[P.num_seqs], tot_part = P.off_part[P.num_seqs];
-  int r, g, k;
+  // the item's work-list entry: all 8 words in one scalar load, so that the
+  // exit test and the item's fields cost a single round trip (the list is
+  // read-only for the whole launch)
+  typedef int int8v __attribute__((ext_vector_type(8)));
+  const int32_t* ep = P.items + (int64_t)blockIdx.x * kItemInts;
+  int8v ev;
+  asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(ev) : "s"(ep) : "memory");
+  const int4 e0 = int4{ev[0], ev[1], ev[2], ev[3]}, e1 = int4{ev[4], ev[5], ev[6], ev[7]};
+  const int r = e0.x;
+  if (r < 0) return;
+  const int g = e0.y, k = e0.z;
   Req R;
-  if (i < tot_full) {
-    r = find_req(P.off_full, P.num_seqs, i);
-    R = load_req(P, r);
-    const int local = i - P.off_full[r];
-    const int nfull = R.n / kSplitKeys;
-    g = uni(local / nfull);
-    k = uni(local % nfull);
-  } else if (i < tot_full + tot_part) {
-    const int j = i - tot_full;
-    r = find_req(P.off_part, P.num_seqs, j);
-    R = load_req(P, r);
-    g = uni(j - P.off_part[r]);
-    k = uni(R.n / kSplitKeys);
-  } else {
-    return;
-  }
+  R.n = e0.w;
+  R.q0 = e1.x;
+  R.s = e1.y;
+  R.valid = true;
   // column blocks actually used by this request: one wave-uniform dispatch
   if (NB == 2 && R.s * P.G > 16)
     split_item<D, NB>(P, r, g, k, R);
@@ -598,14 +677,14 @@ __global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
 // ---------------------------------------------------------------------------
 // chunk kernel: one workgroup (4 wavefronts x 32 columns) per
 // (request, KV head, 128 query-head rows).  The request's K/V tiles stream
-// through a 3-stage LDS ring filled by direct global-to-LDS loads: while the
-// wavefronts compute tile t, the loads of tiles t + 1 and t + 2 are in
-// flight.  The splits are folded in registers as each one ends.
+// through an LDS ring (kChunkStages tiles) filled by direct global-to-LDS
+// loads: while the wavefronts compute tile t, the loads of the next tiles are
+// in flight.  The splits are folded in registers as each one ends.
 // ---------------------------------------------------------------------------
 // Depth of the chunk kernel's LDS ring: tiles t + 1 .. t + kChunkStages - 1 are
 // in flight while tile t is computed.
 #ifndef VD_CHUNK_STAGES
-#define VD_CHUNK_STAGES 3
+#define VD_CHUNK_STAGES 2
 #endif
 constexpr int kChunkStages = VD_CHUNK_STAGES;
 
@@ -642,7 +721,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void chunk_kernel(Params P) {
+// Two workgroups per CU (waves_per_eu 2: at most 256 registers per lane, and
+// two LDS rings of kChunkStages tiles): while one wavefront of a SIMD waits on
+// its softmax chain, the other issues matrix-core work.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void chunk_kernel(Params P) {
   constexpr int NB = 2;
   constexpr int BLK = kPage * D;                   // elements of one page block
   constexpr int NBLK = 2 * kPagesPerTile;          // 4 K blocks then 4 V blocks
@@ -873,11 +955,12 @@ size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 
 struct WsLayout {
-  size_t off_full, off_part, off_chunk, m_off, z_off, u_off, total;
+  size_t off_full, off_part, off_chunk, items, m_off, z_off, u_off, total;
 };
 
-// Workspace: three offset arrays of num_seqs + 1 int32, then the split
-// partial states (m, z, U) for every (request, KV head, column < 32, split).
+// Workspace: three offset arrays of num_seqs + 1 int32, the split work list
+// (8 int32 per grid slot of the split launch), then the split partial states
+// (m, z, U) for every (request, KV head, column < 32, split).
 WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_context_len) {
   const int64_t ms = ((int64_t)max_context_len + kSplitKeys - 1) / kSplitKeys;
   const int64_t n = (int64_t)num_seqs * h->hkv * kSplitCols * (ms < 1 ? 1 : ms);
@@ -886,7 +969,8 @@ WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_context_len) 
   L.off_full = 0;
   L.off_part = offs;
   L.off_chunk = 2 * offs;
-  L.m_off = 3 * offs;
+  L.items = 3 * offs;
+  L.m_off = L.items + round_up((size_t)num_seqs * h->hkv * (ms < 1 ? 1 : ms) * kItemInts * sizeof(int32_t));
   L.z_off = L.m_off + round_up(n * sizeof(float));
   L.u_off = L.z_off + round_up(n * sizeof(float));
   L.total = L.u_off + round_up((size_t)n * h->d * sizeof(float));
@@ -924,6 +1008,7 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.off_full = reinterpret_cast<int32_t*>(w + L.off_full);
   P.off_part = reinterpret_cast<int32_t*>(w + L.off_part);
   P.off_chunk = reinterpret_cast<int32_t*>(w + L.off_chunk);
+  P.items = reinterpret_cast<int32_t*>(w + L.items);
   P.ws_m = reinterpret_cast<float*>(w + L.m_off);
   P.ws_z = reinterpret_cast<float*>(w + L.z_off);
   P.ws_u = reinterpret_cast<float*>(w + L.u_off);
