@@ -9,8 +9,9 @@ behind by the previous step.
 
 Prints one JSON line: whole-step KV GB/s (algorithmic K+V bytes of the batch
 over the step time), the roofline of the dominant kernel measured with HIP
-events on the launch stream, and the CPU oracle timed on the host as a
-reported baseline.
+events on the launch stream (recorded by that kernel's own dispatch, so that
+no marker packet sits between the step's kernels), and the CPU oracle timed
+on the host as a reported baseline.
 """
 from __future__ import annotations
 
@@ -130,6 +131,9 @@ def main():
     ap.add_argument("--workload", default="decode8b", choices=sorted(workloads()))
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--time-every", type=int, default=4,
+                    help="time the dominant kernel with HIP events on every N-th timed step "
+                         "(each timed launch costs the stream a few microseconds)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one plain copy kernel of this many MiB (float32 negate: reads "
                          "and writes that many bytes) before timing, to calibrate HBM counters")
@@ -175,41 +179,46 @@ def main():
     G = sh.group
     chunk_flops = sum(sum(p + 1 for p in r.positions) for r in call.reqs
                       if r.s * G > 32) * sh.num_q_heads * sh.head_dim * 4
-    split_reqs = [r for r in call.reqs if r.s * G <= 32]
-    split_bytes = sum(r.n for r in split_reqs) * sh.num_kv_heads * sh.head_dim * 4
+    split_idx = [i for i, r in enumerate(call.reqs) if r.s * G <= 32]
+    split_reqs = [call.reqs[i] for i in split_idx]
+    # bytes the split kernel must read at least once: distinct cache slots
+    # (pages shared by several requests count once)
+    split_bytes = call.unique_kv_bytes(split_idx)
     # the kernel that bounds the step: compare ideal times on its roofline
     dominant = "chunks" if chunk_flops / (MFMA_BF16_PEAK_TFS * 1e12) > \
         split_bytes / (HBM_PEAK_GBS * 1e9) else "splits"
 
+    # each replica's call marshalled once: a phase is then a single C call
+    prepared = [attn.prepare(dc.batch, out, ws, stream) for dc, ws, out in reps]
+
     def step(i, ev=None, all_ev=None):
-        dc, ws, out = reps[i % len(reps)]
-        b = dc.batch
-        phases = [
-            lambda: attn.forward_plan(b, ws, stream=stream),
-            lambda: attn.forward_splits(b, out, ws, stream=stream),
-            lambda: attn.forward_chunks(b, out, ws, stream=stream),
-            lambda: attn.forward_merge(b, out, ws, stream=stream),
-        ]
+        pc = prepared[i % len(prepared)]
+        phases = [pc.plan, pc.splits, pc.chunks, pc.merge]
         names = ["plan_and_kv_write", "splits", "chunks", "merge"]
         for j, (name, fn) in enumerate(zip(names, phases)):
             if all_ev is not None:
                 all_ev[j].record(stream)
             if ev is not None and name == dominant:
-                ev[0].record(stream)
-            fn()
-            if ev is not None and name == dominant:
-                ev[1].record(stream)
+                fn(events=ev)  # recorded by the kernel's own dispatch
+            else:
+                fn()
         if all_ev is not None:
             all_ev[len(phases)].record(stream)
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    every = max(args.time_every, 1)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+           for _ in range(0, args.steps, every)]
+    for pair in evs:  # create the HIP events before the timed region
+        for e in pair:
+            e.record(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, ev=evs[i])
+        step(args.warmup + i, ev=evs[i // every] if i % every == 0 else None)
+    enqueued = time.perf_counter() - t0
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms = elapsed * 1e3 / args.steps
@@ -220,10 +229,12 @@ def main():
         step(i, all_ev=diag[i])
     torch.cuda.synchronize()
     ph_ms = np.mean([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in diag], axis=0)
-    log("timed: %.4f ms/step, %s kernel %.4f ms; diagnostic phases (ms): plan+kv_write %.4f "
-        "splits %.4f chunks %.4f merge %.4f" % (ms, dominant, dom_ms, *ph_ms))
+    log("timed: %.4f ms/step (enqueue %.4f), %s kernel %.4f ms; diagnostic phases (ms): "
+        "plan+kv_write %.4f splits %.4f chunks %.4f merge %.4f"
+        % (ms, enqueued * 1e3 / args.steps, dominant, dom_ms, *ph_ms))
 
     kv_bytes = call.kv_bytes()
+    uniq_bytes = call.unique_kv_bytes()
     T = call.total_q_tokens
     hq, hkv, D = sh.num_q_heads, sh.num_kv_heads, sh.head_dim
     value = kv_bytes / (ms * 1e-3) / 1e9
@@ -233,7 +244,8 @@ def main():
                 "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
                 "frac": round(ach / MFMA_BF16_PEAK_TFS, 4),
                 "traffic": measured_traffic("chunk_kernel", args.workload),
-                "avg_ms": round(dom_ms, 5), "algorithmic_flop": int(chunk_flops)}
+                "avg_ms": round(dom_ms, 5), "timed_launches": len(evs),
+                "algorithmic_flop": int(chunk_flops)}
     else:
         alg = split_bytes + sum(r.s for r in split_reqs) * hq * D * 2 + \
             sum(-(-r.n // P) for r in split_reqs) * 4
@@ -241,7 +253,8 @@ def main():
         roof = {"kernel": "split_kernel", "bound": "hbm", "achieved": round(ach, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic("split_kernel", args.workload),
-                "avg_ms": round(dom_ms, 5), "algorithmic_bytes": int(alg)}
+                "avg_ms": round(dom_ms, 5), "timed_launches": len(evs),
+                "algorithmic_bytes": int(alg)}
 
     res = {
         "metric": "paged-attn KV GB/s (% HBM peak) at bitwise batch/chunk/page invariance",
@@ -257,9 +270,14 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": desc, "num_seqs": call.num_seqs, "query_rows": T,
-                   "kv_bytes": kv_bytes, "replicas": len(reps)},
-        "hbm_frac_whole_step": round(value / HBM_PEAK_GBS, 4),
+                   "kv_bytes": kv_bytes, "kv_bytes_distinct": uniq_bytes,
+                   "replicas": len(reps)},
+        # distinct K+V bytes of the call over the step time, against HBM peak
+        "hbm_frac_whole_step": round(uniq_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "tokens_per_s": round(T / (ms * 1e-3), 1),
+        # host time to enqueue the timed steps: well below ms_per_step means
+        # the GPU, not the launch path, set the pace
+        "enqueue_ms_per_step": round(enqueued * 1e3 / args.steps, 5),
         "phase_ms_diagnostic": {k: round(float(v), 5) for k, v in
                                 zip(["plan_and_kv_write", "splits", "chunks", "merge"], ph_ms)},
         "roofline": roof,

@@ -157,6 +157,19 @@ int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* batch, void* o
 int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* batch, void* out,
                           const void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The splits and chunks phases with their kernel timed: identical launches
+ * and results, and in addition `start` and `stop` (hipEvent_t the caller
+ * created with timing enabled, or NULL) are recorded by the kernel's own
+ * dispatch (hipExtLaunchKernel) at its start and end, with no separate marker
+ * packet in the stream.  When the phase launches no kernel (no such rows),
+ * both events are recorded back to back on `stream`. */
+int vd_attn_forward_splits_timed(const vd_attn* h, const vd_attn_batch* batch, void* out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                 hipEvent_t start, hipEvent_t stop);
+int vd_attn_forward_chunks_timed(const vd_attn* h, const vd_attn_batch* batch, void* out,
+                                 const void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream, hipEvent_t start, hipEvent_t stop);
+
 /* Bytes of ONE pool (K or V) holding num_pages pages. */
 int vd_pool_bytes(const vd_attn* h, int64_t num_pages, size_t* bytes);
 

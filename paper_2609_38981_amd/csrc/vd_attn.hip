@@ -22,6 +22,7 @@
 //                 and writes the output rows of the split-path requests.
 // The work decomposition differs between kernels; the operations applied to
 // any one output row, and their order (vd_cas.hpp), do not.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -1045,16 +1046,18 @@ int run_plan(const Params& P, hipStream_t s) {
   return launched();
 }
 
+// Kernel launches go through hipExtLaunchKernelGGL, which records the
+// optional timing events e0 / e1 with the dispatch itself.
 template <int D>
-int run_splits(const Params& P, hipStream_t s) {
+int run_splits(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
   // upper bound of the split items; items past the planned total exit at once
   const int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
   if (items > INT32_MAX - 4) return VD_ERR_INVALID_ARG;
   const dim3 grid((unsigned)items), block(64);
   if (P.split_cols == 16)
-    hipLaunchKernelGGL((split_kernel<D, 1>), grid, block, 0, s, P);
+    hipExtLaunchKernelGGL((split_kernel<D, 1>), grid, block, 0, s, e0, e1, 0, P);
   else
-    hipLaunchKernelGGL((split_kernel<D, 2>), grid, block, 0, s, P);
+    hipExtLaunchKernelGGL((split_kernel<D, 2>), grid, block, 0, s, e0, e1, 0, P);
   return launched();
 }
 
@@ -1077,7 +1080,7 @@ int run_merge(const Params& P, hipStream_t s) {
 }
 
 template <int D>
-int run_chunks(const Params& P, hipStream_t s) {
+int run_chunks(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
   // upper bound of sum_r Hkv * ceil(s_r G / 128) <= Hkv (ceil(T G / 128) + B),
   // rounded up to a multiple of the 8 XCDs
   int64_t blocks = (int64_t)P.hkv * ((P.T * P.G + kChunkCols - 1) / kChunkCols + P.num_seqs);
@@ -1088,7 +1091,8 @@ int run_chunks(const Params& P, hipStream_t s) {
       reinterpret_cast<const void*>(&chunk_kernel<D>), hipFuncAttributeMaxDynamicSharedMemorySize,
       (int)lds);
   if (attr != hipSuccess) return VD_ERR_LAUNCH;
-  hipLaunchKernelGGL((chunk_kernel<D>), dim3((unsigned)blocks), dim3(256), lds, s, P);
+  hipExtLaunchKernelGGL((chunk_kernel<D>), dim3((unsigned)blocks), dim3(256), (uint32_t)lds, s, e0,
+                        e1, 0, P);
   return launched();
 }
 
@@ -1173,6 +1177,40 @@ int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* b, void* out,
   if (!needs_chunks(h, b)) return VD_OK;
   const Params P = make_params(h, b, out, workspace);
   return h->d == 64 ? run_chunks<64>(P, stream) : run_chunks<128>(P, stream);
+}
+
+// Events of a phase that launches nothing: recorded back to back.
+static int record_pair(hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (e0 && hipEventRecord(e0, s) != hipSuccess) return VD_ERR_LAUNCH;
+  if (e1 && hipEventRecord(e1, s) != hipSuccess) return VD_ERR_LAUNCH;
+  return VD_OK;
+}
+
+int vd_attn_forward_splits_timed(const vd_attn* h, const vd_attn_batch* b, void* out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                 hipEvent_t start, hipEvent_t stop) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK) return rc;
+  if (b->num_seqs == 0 || b->total_q_tokens == 0) return record_pair(stream, start, stop);
+  if (!out) return VD_ERR_INVALID_ARG;
+  if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
+  const Params P = make_params(h, b, out, workspace);
+  return h->d == 64 ? run_splits<64>(P, stream, start, stop)
+                    : run_splits<128>(P, stream, start, stop);
+}
+
+int vd_attn_forward_chunks_timed(const vd_attn* h, const vd_attn_batch* b, void* out,
+                                 const void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK) return rc;
+  if (b->num_seqs == 0 || b->total_q_tokens == 0) return record_pair(stream, start, stop);
+  if (!out) return VD_ERR_INVALID_ARG;
+  if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
+  if (!needs_chunks(h, b)) return record_pair(stream, start, stop);
+  const Params P = make_params(h, b, out, workspace);
+  return h->d == 64 ? run_chunks<64>(P, stream, start, stop)
+                    : run_chunks<128>(P, stream, start, stop);
 }
 
 int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* b, void* out,

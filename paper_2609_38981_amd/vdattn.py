@@ -77,6 +77,10 @@ def load_library(path: str = LIB_PATH):
         "vd_attn_forward_splits": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_attn_forward_chunks": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_attn_forward_merge": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
+        "vd_attn_forward_splits_timed": (ctypes.c_int,
+                                         [P, ctypes.POINTER(_Batch), P, P, SZ, P, P, P]),
+        "vd_attn_forward_chunks_timed": (ctypes.c_int,
+                                         [P, ctypes.POINTER(_Batch), P, P, SZ, P, P, P]),
         "vd_pool_bytes": (ctypes.c_int, [P, I64, ctypes.POINTER(SZ)]),
         "vd_kv_write": (ctypes.c_int, [P, P, P, P, I64, P, P, I64, P]),
         "vd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -280,6 +284,11 @@ class VdAttn:
         _check(self.lib.vd_attn_forward_merge(self._h, ctypes.byref(cb), _ptr(out), _ptr(ws),
                                               ws.numel(), _stream(stream)), "vd_attn_forward_merge")
 
+    def prepare(self, b: Batch, out=None, workspace=None, stream=None) -> "PreparedCall":
+        """Marshals one call's arguments once, for callers that launch the same
+        call (same tensors, same stream) many times."""
+        return PreparedCall(self, b, out, workspace, stream)
+
     def kv_write(self, k_new: torch.Tensor, v_new: torch.Tensor, slot_mapping: torch.Tensor,
                  k_pool: torch.Tensor, v_pool: torch.Tensor, num_pages: int, stream=None):
         T = int(slot_mapping.numel())
@@ -293,3 +302,64 @@ class VdAttn:
         _check(self.lib.vd_kv_write(self._h, _ptr(k_new), _ptr(v_new), _ptr(slot_mapping), T,
                                     _ptr(k_pool), _ptr(v_pool), int(num_pages), _stream(stream)),
                "vd_kv_write")
+
+
+class PreparedCall:
+    """The C arguments of one attention call, checked and marshalled once.
+
+    Holds references to every tensor it points at.  Each method is one C call
+    with those arguments; the phases compose exactly like forward()."""
+
+    def __init__(self, attn: VdAttn, b: Batch, out=None, workspace=None, stream=None):
+        self.attn, self.batch = attn, b
+        self.cb = attn._batch(b)
+        self.out = attn._out(b, out)
+        self.workspace = attn._ws(b, workspace)
+        self.stream = stream
+        lib, h = attn.lib, attn._h
+        pcb, sp = ctypes.byref(self.cb), _stream(stream)
+        o, w, wn = _ptr(self.out), _ptr(self.workspace), self.workspace.numel()
+        self._fwd = (lib.vd_attn_forward, (h, pcb, o, w, wn, sp))
+        self._plan = (lib.vd_attn_forward_plan, (h, pcb, w, wn, sp))
+        self._splits = (lib.vd_attn_forward_splits, (h, pcb, o, w, wn, sp))
+        self._chunks = (lib.vd_attn_forward_chunks, (h, pcb, o, w, wn, sp))
+        self._merge = (lib.vd_attn_forward_merge, (h, pcb, o, w, wn, sp))
+        self._splits_timed = (lib.vd_attn_forward_splits_timed, (h, pcb, o, w, wn, sp))
+        self._chunks_timed = (lib.vd_attn_forward_chunks_timed, (h, pcb, o, w, wn, sp))
+
+    @staticmethod
+    def _run(fa, what):
+        fn, args = fa
+        _check(fn(*args), what)
+
+    def forward(self) -> torch.Tensor:
+        self._run(self._fwd, "vd_attn_forward")
+        return self.out
+
+    def plan(self):
+        self._run(self._plan, "vd_attn_forward_plan")
+
+    @staticmethod
+    def _timed(fa, events, what):
+        """events: a pair of torch.cuda.Event(enable_timing=True); the kernel's
+        dispatch records them at its start and end."""
+        fn, args = fa
+        for e in events:
+            if not e.cuda_event:  # torch creates the event at its first record
+                e.record()
+        _check(fn(*args, events[0].cuda_event, events[1].cuda_event), what)
+
+    def splits(self, events=None):
+        if events is None:
+            self._run(self._splits, "vd_attn_forward_splits")
+        else:
+            self._timed(self._splits_timed, events, "vd_attn_forward_splits_timed")
+
+    def chunks(self, events=None):
+        if events is None:
+            self._run(self._chunks, "vd_attn_forward_chunks")
+        else:
+            self._timed(self._chunks_timed, events, "vd_attn_forward_chunks_timed")
+
+    def merge(self):
+        self._run(self._merge, "vd_attn_forward_merge")

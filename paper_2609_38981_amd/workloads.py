@@ -241,6 +241,21 @@ class Call:
         sh = self.shape
         return int(sum(r.n for r in self.reqs)) * sh.num_kv_heads * sh.head_dim * 2 * 2
 
+    def unique_kv_bytes(self, req_indices=None) -> int:
+        """K+V bytes of the distinct cache slots the given requests (default:
+        all) read: a page shared by several requests counts once, with the
+        largest number of its slots any of them reads."""
+        sh = self.shape
+        P = sh.page_size
+        idx = range(len(self.reqs)) if req_indices is None else req_indices
+        used = {}
+        for ri in idx:
+            n = int(self.context_lens[ri])
+            for lp in range(-(-n // P)):
+                page = int(self.page_table[ri, lp])
+                used[page] = max(used.get(page, 0), min(P, n - lp * P))
+        return int(sum(used.values())) * sh.num_kv_heads * sh.head_dim * 2 * 2
+
     def new_tokens(self) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
         """This call's own tokens (positions n - s .. n - 1 of every request):
         (k_rows, v_rows [N, Hkv, D] uint16, slot ids int64 [N])."""

@@ -39,8 +39,10 @@ def handle(shape: W.Shape) -> VdAttn:
 
 
 def gpu_run(call: W.Call, poison: bool = True, stream=None, workspace_fill=None,
-            **kw) -> np.ndarray:
-    """Output bits (uint16 [T, Hq, D]) of one vd_attn_forward call."""
+            prepared=None, **kw) -> np.ndarray:
+    """Output bits (uint16 [T, Hq, D]) of one vd_attn_forward call (or, with
+    prepared = "forward" / "phases" / "timed", of a prepared call run whole, phase
+    by phase, or phase by phase with the kernels' dispatches recording events)."""
     attn = handle(call.shape)
     dc = S.to_device(attn, call, poison=poison, **kw)
     ws = attn.new_workspace(call.num_seqs, dc.batch.max_q_len, dc.batch.max_context_len)
@@ -48,7 +50,25 @@ def gpu_run(call: W.Call, poison: bool = True, stream=None, workspace_fill=None,
         ws.view(torch.int8).fill_(workspace_fill)
     out = torch.empty_like(dc.batch.q)
     out.view(torch.int16).fill_(0x7FC0)
-    if stream is None:
+    if prepared is not None:
+        pc = attn.prepare(dc.batch, out, ws)
+        if prepared == "forward":
+            pc.forward()
+        elif prepared == "timed":
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            pc.plan()
+            pc.splits(events=ev[:2])
+            pc.chunks(events=ev[2:])
+            pc.merge()
+            torch.cuda.synchronize()
+            for a, b in (ev[:2], ev[2:]):
+                assert a.elapsed_time(b) >= 0.0
+        else:
+            pc.plan()
+            pc.splits()
+            pc.chunks()
+            pc.merge()
+    elif stream is None:
         attn.forward(dc.batch, out=out, workspace=ws)
     else:
         with torch.cuda.stream(stream):

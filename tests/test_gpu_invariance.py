@@ -101,7 +101,8 @@ def test_probe_request_batch_invariance():
 
 def test_metadata_does_not_matter():
     """Oversized hints, a wider page-table stride, a bigger pool, a NaN-filled
-    workspace, another stream and a repeat run give the same bits."""
+    workspace, another stream, a repeat run and a prepared call (whole or
+    phase by phase) give the same bits."""
     mk = lambda **kw: W.config2(batch=9, lo=300, hi=1800, **kw)
     base = outs(mk())
     call = mk()
@@ -111,6 +112,9 @@ def test_metadata_does_not_matter():
         "ws_nan": dict(workspace_fill=-1),
         "stream": dict(stream=torch.cuda.Stream()),
         "repeat": {},
+        "prepared_forward": dict(prepared="forward"),
+        "prepared_phases": dict(prepared="phases"),
+        "prepared_timed": dict(prepared="timed"),
     }
     for name, kw in variants.items():
         U.assert_same_bits(base, U.by_position(call, U.gpu_run(call, **kw)), min_common=9)
@@ -121,11 +125,15 @@ def test_metadata_does_not_matter():
 
 def test_mixed_batch_orders():
     """Config 3 family: prefill chunks and decodes in one call, rows ordered
-    prefill-first or shuffled, give the same bits."""
+    prefill-first or shuffled, and the timed phase launches, give the same
+    bits."""
     kw = dict(num_prefill=3, chunk=96, max_off=900, num_decode=10, dec_lo=60, dec_hi=1500)
     a = outs(W.config3(**kw))
     b = outs(W.config3(shuffle=True, perm_stream=5, **kw))
     U.assert_same_bits(a, b, min_common=3 * 96 + 10)
+    # the timed split and chunk launches compute the same bits
+    c = outs(W.config3(**kw), prepared="timed")
+    U.assert_same_bits(a, c, min_common=3 * 96 + 10)
 
 
 def test_prefix_sharing_and_verify_steps():
