@@ -205,6 +205,15 @@ def main():
         if all_ev is not None:
             all_ev[len(phases)].record(stream)
 
+    if args.copy_calibration_mb:
+        # one plain copy kernel of known size, for scaling the HBM counters
+        n = (args.copy_calibration_mb << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
