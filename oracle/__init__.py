@@ -57,7 +57,7 @@ def bind(path: str):
     lib.vdo_paged_attention.restype = ctypes.c_int
     lib.vdo_paged_attention.argtypes = [
         ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-        ctypes.c_int, ctypes.c_double, P, P, P, P, ctypes.c_int, P, P,
+        ctypes.c_int, ctypes.c_double, ctypes.c_int, P, P, P, P, ctypes.c_int, P, P,
         ctypes.c_int64, P, P, ctypes.c_int]
     lib.vdo_default_threads.restype = ctypes.c_int
     return lib
@@ -83,7 +83,7 @@ def _c(a, dtype):
 
 def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_pool_bits,
                     *, num_q_heads, num_kv_heads, head_dim, page_size, scale=None,
-                    rows=None, threads=0, lib=None) -> np.ndarray:
+                    window=0, rows=None, threads=0, lib=None) -> np.ndarray:
     """Exact (fp64) paged causal attention.
 
     q_bits:        uint16 [T, Hq, D] bf16 bit patterns, rows packed by request.
@@ -92,6 +92,8 @@ def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_
     page_table:    int32 [B, stride]; the first ceil(n_r / P) entries are used.
     k/v_pool_bits: uint16 [num_pages, Hkv, P, D] bf16 bit patterns.
     scale:         softmax scale (default 1/sqrt(D)).
+    window:        0 for the full causal prefix; w > 0 restricts row p to the
+                   sliding window of keys p - w < j <= p (Appendix A.5).
     rows:          optional iterable of token indices (or bool mask [T]); only
                    those rows are computed, the rest of the result is NaN.
     threads:       host threads (0 = all online cores).
@@ -128,9 +130,9 @@ def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_
         sel, selp = _c(sel, np.uint8)
     out = np.full((T, num_q_heads, head_dim), np.nan, np.float64)
     rc = lib.vdo_paged_attention(
-        B, T, num_q_heads, num_kv_heads, head_dim, page_size, float(scale), qp, cup, ctxp,
-        ptp, stride, kpp, vpp, kp.shape[0], selp, out.ctypes.data_as(ctypes.c_void_p),
-        int(threads))
+        B, T, num_q_heads, num_kv_heads, head_dim, page_size, float(scale), int(window), qp,
+        cup, ctxp, ptp, stride, kpp, vpp, kp.shape[0], selp,
+        out.ctypes.data_as(ctypes.c_void_p), int(threads))
     if rc != 0:
         raise ValueError("oracle rejected the call: %s (%d)" % (ERRORS.get(rc, "?"), rc))
     return out

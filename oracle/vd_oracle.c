@@ -28,6 +28,12 @@
  *   which is exactly softmax attention restricted to the causal prefix
  *   j <= p (the mask of Appendix A.2 reduces to j <= p because p < n).
  *
+ *   Sliding-window attention (Appendix A.5, "Relational Alignment and
+ *   Composition"): with a window size w > 0 shared by the call, key j is
+ *   visible to position p only when also j > p - w, so the sums above run
+ *   over j = max(0, p - w + 1) .. p.  w = 0 means no window (the full
+ *   causal prefix).
+ *
  * Every sum runs in ascending index order in double precision.  No blocking,
  * no online softmax, no splitting: the definition written out.
  *
@@ -60,6 +66,7 @@ typedef struct {
   int64_t total_q_tokens;
   int hq, hkv, d, page_size;
   double scale;
+  int window; /* 0: full causal prefix; w > 0: keys p - w < j <= p */
   const uint16_t *q;
   const int32_t *cu_q_lens, *context_lens, *page_table;
   int pt_stride;
@@ -86,10 +93,12 @@ static int run_item(job_t *J, int r, int h, double *score, double *w) {
     const int64_t t = (int64_t)q0 + i;
     if (J->row_select && !J->row_select[t]) continue;
     const int p = n - s + i; /* logical position of this row */
+    /* first visible key: 0, or the start of the sliding window */
+    const int lo = (J->window > 0 && p - J->window + 1 > 0) ? p - J->window + 1 : 0;
     const uint16_t *qrow = J->q + (t * J->hq + h) * (int64_t)D;
 
-    /* scores over the causal prefix j = 0..p */
-    for (int j = 0; j <= p; ++j) {
+    /* scores over the visible keys j = lo..p */
+    for (int j = lo; j <= p; ++j) {
       const int64_t page = pt[j / P];
       const uint16_t *krow =
           J->k_pool + (((page * J->hkv + g) * P) + (j % P)) * (int64_t)D;
@@ -100,18 +109,18 @@ static int run_item(job_t *J, int r, int h, double *score, double *w) {
     }
     /* softmax */
     double mx = -INFINITY;
-    for (int j = 0; j <= p; ++j)
+    for (int j = lo; j <= p; ++j)
       if (score[j] > mx) mx = score[j];
     double denom = 0.0;
-    for (int j = 0; j <= p; ++j) {
+    for (int j = lo; j <= p; ++j) {
       w[j] = exp(score[j] - mx);
       denom += w[j];
     }
-    for (int j = 0; j <= p; ++j) w[j] /= denom;
+    for (int j = lo; j <= p; ++j) w[j] /= denom;
     /* weighted sum of values */
     double *orow = J->out + (t * J->hq + h) * (int64_t)D;
     for (int dd = 0; dd < D; ++dd) orow[dd] = 0.0;
-    for (int j = 0; j <= p; ++j) {
+    for (int j = lo; j <= p; ++j) {
       const int64_t page = pt[j / P];
       const uint16_t *vrow =
           J->v_pool + (((page * J->hkv + g) * P) + (j % P)) * (int64_t)D;
@@ -149,7 +158,8 @@ static void *worker(void *arg) {
 /* Validates the logical inputs before anything is computed. */
 static int validate(const job_t *J) {
   if (J->num_seqs < 0 || J->hq <= 0 || J->hkv <= 0 || J->d <= 0 ||
-      J->page_size <= 0 || J->hq % J->hkv != 0 || J->pt_stride < 0)
+      J->page_size <= 0 || J->hq % J->hkv != 0 || J->pt_stride < 0 ||
+      J->window < 0)
     return VDO_ERR_ARG;
   if (J->cu_q_lens[0] != 0 || J->cu_q_lens[J->num_seqs] != J->total_q_tokens)
     return VDO_ERR_LENGTHS;
@@ -167,9 +177,10 @@ static int validate(const job_t *J) {
   return VDO_OK;
 }
 
+/* window: 0 for the full causal prefix, w > 0 for a sliding window of w keys */
 int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
                         int num_kv_heads, int head_dim, int page_size,
-                        double scale, const uint16_t *q,
+                        double scale, int window, const uint16_t *q,
                         const int32_t *cu_q_lens, const int32_t *context_lens,
                         const int32_t *page_table, int pt_stride,
                         const uint16_t *k_pool, const uint16_t *v_pool,
@@ -187,6 +198,7 @@ int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
   J.d = head_dim;
   J.page_size = page_size;
   J.scale = scale;
+  J.window = window;
   J.q = q;
   J.cu_q_lens = cu_q_lens;
   J.context_lens = context_lens;

@@ -6,14 +6,17 @@ disagrees with the fact it is pinned to:
 
 * a library routine: ``torch.nn.functional.scaled_dot_product_attention`` in
   float64 (causal prefill, a chunk at a key offset via an explicit ``tril``
-  mask, grouped-query heads via ``enable_gqa``), and ``scipy.special.softmax``;
-* closed forms: a single visible key returns that key's value exactly; a zero
-  query or identical keys give the plain mean of the visible values; one
-  dominant score returns (nearly) that key's value;
+  mask, grouped-query heads via ``enable_gqa``, a sliding window via a banded
+  mask), and ``scipy.special.softmax``;
+* closed forms: a single visible key (n = 1, row 0, or a window of 1) returns
+  that key's value exactly; a zero query or identical keys give the plain mean
+  of the visible values (the prefix, or the window); one dominant score
+  returns (nearly) that key's value;
 * the paper's worked example of Fig. 4 (golden fixture);
 * invariants the paper requires of the attention result: physical page
   placement, prompt chunking, batch composition and order, and data at
-  positions after p (causal masking) do not change a row.
+  positions after p (causal masking) or before the window do not change a
+  row; a window covering the prefix is full attention.
 """
 from __future__ import annotations
 
@@ -65,10 +68,10 @@ def pack(reqs, hq, hkv, d, P, num_pages=None, rng=None, pages=None, poison=True)
     return q, cu, ctx, pt, kp, vp
 
 
-def run(lib, reqs, hq, hkv, d, P, scale=None, **kw):
+def run(lib, reqs, hq, hkv, d, P, scale=None, window=0, **kw):
     q, cu, ctx, pt, kp, vp = pack(reqs, hq, hkv, d, P, **kw)
     return oracle.paged_attention(q, cu, ctx, pt, kp, vp, num_q_heads=hq, num_kv_heads=hkv,
-                                  head_dim=d, page_size=P, scale=scale, lib=lib)
+                                  head_dim=d, page_size=P, scale=scale, window=window, lib=lib)
 
 
 def rand_req(rng, s, n, hq, hkv, d):
@@ -80,13 +83,17 @@ def f64(bits):
     return W.bf16_to_f32(bits).astype(np.float64)
 
 
-def sdpa_reference(req, hq, hkv, scale=None):
-    """Library attention for one request, rows at positions n - s .. n - 1."""
+def sdpa_reference(req, hq, hkv, scale=None, window=0):
+    """Library attention for one request, rows at positions n - s .. n - 1;
+    with window w > 0 the mask is the band tril(n - s) minus tril(n - s - w)
+    (the sliding window of Appendix A.5)."""
     q = torch.from_numpy(f64(req["q"])).permute(1, 0, 2)[None]  # [1, hq, s, d]
     k = torch.from_numpy(f64(req["k"])).permute(1, 0, 2)[None]  # [1, hkv, n, d]
     v = torch.from_numpy(f64(req["v"])).permute(1, 0, 2)[None]
     s, n = q.shape[2], k.shape[2]
     mask = torch.ones(s, n, dtype=torch.bool).tril(diagonal=n - s)
+    if window > 0:
+        mask &= ~torch.ones(s, n, dtype=torch.bool).tril(diagonal=n - s - window)
     o = F.scaled_dot_product_attention(q, k, v, attn_mask=mask, enable_gqa=(hq != hkv), scale=scale)
     return o[0].permute(1, 0, 2).numpy()  # [s, hq, d]
 
@@ -249,9 +256,76 @@ def pin_invariances(lib):
             assert np.array_equal(val, base[key]), key
 
 
+# -- sliding window (Appendix A.5: key j visible to p when p - w < j <= p) ----
+def pin_sdpa_window(lib):
+    """Chunks at key offsets with a sliding window equal SDPA with a banded
+    causal mask (GQA, scattered pages, windows shorter and longer than s)."""
+    rng = np.random.default_rng(21)
+    hq, hkv, d, P = 8, 2, 32, 16
+    for w in (3, 16, 40):
+        reqs = [rand_req(rng, s, n, hq, hkv, d) for s, n in [(1, 37), (8, 100), (5, 5), (20, 61)]]
+        got = run(lib, reqs, hq, hkv, d, P, window=w)
+        off = 0
+        for r in reqs:
+            s = r["q"].shape[0]
+            np.testing.assert_allclose(got[off:off + s], sdpa_reference(r, hq, hkv, window=w),
+                                       rtol=0, atol=1e-12)
+            off += s
+
+
+def pin_window_one_key(lib):
+    """w = 1 leaves one visible key: every row returns v_p bit for bit."""
+    rng = np.random.default_rng(22)
+    hq, hkv, d, P = 4, 2, 16, 4
+    req = rand_req(rng, 6, 19, hq, hkv, d)
+    got = run(lib, [req], hq, hkv, d, P, window=1)
+    v = f64(req["v"])
+    for i in range(6):
+        for h in range(hq):
+            assert np.array_equal(got[i, h], v[13 + i, h // 2])
+
+
+def pin_window_zero_query_mean(lib):
+    """q = 0 gives the mean of the window's values v_(p-w+1)..v_p."""
+    rng = np.random.default_rng(23)
+    hq, hkv, d, P, w = 2, 1, 16, 4, 7
+    req = rand_req(rng, 10, 30, hq, hkv, d)
+    req["q"][:] = 0
+    got = run(lib, [req], hq, hkv, d, P, window=w)
+    v = f64(req["v"])
+    for i in range(10):
+        p = 20 + i
+        for h in range(hq):
+            np.testing.assert_allclose(got[i, h], v[p - w + 1:p + 1, 0].mean(axis=0), rtol=0,
+                                       atol=1e-12)
+
+
+def pin_window_limits(lib):
+    """A window covering the whole prefix is full attention bit for bit, and
+    K/V before the window do not change a row (while a row whose window
+    includes them does change)."""
+    rng = np.random.default_rng(24)
+    hq, hkv, d, P = 4, 2, 16, 8
+    req = rand_req(rng, 5, 33, hq, hkv, d)
+    full = run(lib, [req], hq, hkv, d, P)
+    assert np.array_equal(full, run(lib, [req], hq, hkv, d, P, window=33))
+    assert np.array_equal(full, run(lib, [req], hq, hkv, d, P, window=1000))
+    w = 10
+    a = run(lib, [req], hq, hkv, d, P, window=w)
+    alt = {k: v.copy() for k, v in req.items()}
+    alt["k"][:19] = W.normal_bf16(rng, alt["k"][:19].shape)   # rows p >= 28 see keys >= 19
+    alt["v"][:19] = W.normal_bf16(rng, alt["v"][:19].shape)
+    b = run(lib, [alt], hq, hkv, d, P, window=w)
+    assert np.array_equal(a[0], b[0])  # p = 28: window 19..28
+    alt["k"][19] = W.normal_bf16(rng, alt["k"][19].shape)
+    c = run(lib, [alt], hq, hkv, d, P, window=w)
+    assert not np.array_equal(a[0], c[0])
+
+
 ALL_PINS = [pin_sdpa_prefill, pin_sdpa_chunk_offset, pin_sdpa_scale, pin_scipy_softmax_dense,
             pin_single_key, pin_zero_query_mean, pin_identical_keys_mean, pin_dominant_key,
-            pin_fig4_example, pin_invariances]
+            pin_fig4_example, pin_invariances, pin_sdpa_window, pin_window_one_key,
+            pin_window_zero_query_mean, pin_window_limits]
 
 
 if __name__ == "__main__":

@@ -98,8 +98,13 @@ MUTANTS = {
                         "((page * J->hkv + g) * P) + (P - 1 - j % P)) * (int64_t)D;\n      double acc"),
     "unnormalised": ("w[j] /= denom;", "w[j] /= 1.0;"),
     "value_from_key_pool": ("J->v_pool + (((page", "J->k_pool + (((page"),
-    "drops_last_key": ("for (int j = 0; j <= p; ++j) {\n      const int64_t page = pt[j / P];\n      const uint16_t *vrow",
-                       "for (int j = 0; j < p; ++j) {\n      const int64_t page = pt[j / P];\n      const uint16_t *vrow"),
+    "drops_last_key": ("for (int j = lo; j <= p; ++j) {\n      const int64_t page = pt[j / P];\n      const uint16_t *vrow",
+                       "for (int j = lo; j < p; ++j) {\n      const int64_t page = pt[j / P];\n      const uint16_t *vrow"),
+    "window_off_by_one": ("p - J->window + 1 > 0) ? p - J->window + 1 : 0;",
+                          "p - J->window > 0) ? p - J->window : 0;"),
+    "window_ignored": ("const int lo = (J->window > 0 &&", "const int lo = (J->window < 0 &&"),
+    "window_from_n": ("p - J->window + 1 > 0) ? p - J->window + 1 : 0;",
+                      "n - J->window + 1 > 0) ? n - J->window + 1 : 0;"),
 }
 
 
