@@ -51,6 +51,10 @@ def workloads():
                       "Llama-70B prefix-shared verify: 256 requests on a shared 2048-token prefix "
                       "+ suffix U[64,512], s=4 (even) / s=1 (odd), Hq 64 / Hkv 8, head_dim 128"),
         "tiny": (lambda: W.config1(), "tiny: 2 requests (n 37 s 1, n 100 s 8), Hq 4 / Hkv 2, D 64"),
+        "swa8b": (lambda: W.config2(batch=32, lo=8192, hi=32768, shape=W.LLAMA8B_SWA4K, cfg=6,
+                                    pool_factor=1.5),
+                  "Llama-3-8B geometry with a 4096-key sliding window, paged decode: 32 requests, "
+                  "context U[8192,32768], Hq 32 / Hkv 8, head_dim 128, page 16, pool 1.5x need"),
     }
 
 
@@ -106,7 +110,7 @@ def cpu_baseline(call, min_seconds: float = 10.0, max_requests: int = 64):
     kp, vp = call.std_pool(poison=False)
     args = (sub.q_bits(), sub.cu_q_lens, sub.context_lens, sub.page_table, kp, vp)
     kw = dict(num_q_heads=sh.num_q_heads, num_kv_heads=sh.num_kv_heads, head_dim=sh.head_dim,
-              page_size=sh.page_size)
+              page_size=sh.page_size, window=sh.window)
     threads = host_threads()
     reps, t0 = 0, time.perf_counter()
     while True:
@@ -177,7 +181,9 @@ def main():
 
     stream = torch.cuda.current_stream()
     G = sh.group
-    chunk_flops = sum(sum(p + 1 for p in r.positions) for r in call.reqs
+    # visible keys of the row at p: p + 1, or at most the window
+    vis = (lambda p: min(p + 1, sh.window)) if sh.window > 0 else (lambda p: p + 1)
+    chunk_flops = sum(sum(vis(p) for p in r.positions) for r in call.reqs
                       if r.s * G > 32) * sh.num_q_heads * sh.head_dim * 4
     split_idx = [i for i, r in enumerate(call.reqs) if r.s * G <= 32]
     split_reqs = [call.reqs[i] for i in split_idx]
@@ -257,7 +263,7 @@ def main():
                 "algorithmic_flop": int(chunk_flops)}
     else:
         alg = split_bytes + sum(r.s for r in split_reqs) * hq * D * 2 + \
-            sum(-(-r.n // P) for r in split_reqs) * 4
+            sum(-(-r.n // P) - call.first_key(i) // P for i, r in zip(split_idx, split_reqs)) * 4
         ach = alg / (dom_ms * 1e-3) / 1e9
         roof = {"kernel": "split_kernel", "bound": "hbm", "achieved": round(ach, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),

@@ -18,7 +18,8 @@
  *
  * Guarantee (the causal contract of Section 5.3 / Appendix A.1): the output
  * bits of a row depend only on (p, the row's query, K/V at positions 0..p,
- * the handle).  They do not depend on s_r, n_r, the row index, the other
+ * the handle); with a sliding window of w keys (Appendix A.5), only on K/V
+ * at positions max(0, p - w + 1)..p.  They do not depend on s_r, n_r, the row index, the other
  * requests of the call, their order, the page table (physical placement,
  * stride, sharing of pages between requests), num_pages, the hints, the
  * workspace contents or the stream.  Keys are processed in tiles of 64
@@ -58,7 +59,7 @@
 extern "C" {
 #endif
 
-#define VD_ABI_VERSION 1
+#define VD_ABI_VERSION 2
 
 typedef enum {
   VD_OK = 0,
@@ -83,6 +84,10 @@ typedef struct {
   int32_t page_size;    /* P, must be 16 */
   int32_t dtype;        /* VD_DTYPE_BF16: Q, K, V and the output are bf16 */
   float softmax_scale;  /* <= 0 selects 1 / sqrt(head_dim) */
+  int32_t window;       /* sliding-window attention (Appendix A.5, "Relational Alignment and
+                           Composition"): w > 0 restricts the row at position p to the keys
+                           p - w < j <= p; 0 selects the full causal prefix.  Like the scale,
+                           it is fixed by the handle (a model's layer), never by the batch */
 } vd_attn_desc;
 
 typedef struct vd_attn vd_attn; /* opaque, immutable after creation */

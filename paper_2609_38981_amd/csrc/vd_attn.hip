@@ -56,6 +56,7 @@ struct Params {
   int32_t num_pages;  // page ids are int32: pages past INT32_MAX are unreachable
   int num_seqs, pt_stride, max_q, max_ctx, max_splits, split_cols;
   int hq, hkv, G;
+  int window;  // sliding window in keys (Appendix A.5), 0 = the full causal prefix
   float c;  // softmax scale * log2(e), rounded once to fp32 on the host
   // optional new tokens written by the plan launch
   const uint16_t* knew;
@@ -145,6 +146,13 @@ __device__ __forceinline__ void load_q(const Params& P, u16x8 (&qf)[D / 32], int
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks)
     qf[ks] = valid ? *reinterpret_cast<const u16x8*>(base + 32 * ks) : zero8();
+}
+
+// Splits that hold a visible key of some row of request R: from the split of
+// the first row's window start through the split of key n - 1.  When it is
+// one, the split kernel writes the rows; otherwise the merge kernel does.
+__device__ __forceinline__ int request_splits(const Req& R, int window) {
+  return (R.n - 1) / kSplitKeys + 1 - window_lo(R.n - R.s, window) / kSplitKeys;
 }
 
 // Stores one column's output row from its accumulator blocks (lane layout of
@@ -253,9 +261,17 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
       if (R.valid) {
         const int ncols = R.s * P.G;
         if (ncols <= P.split_cols) {
-          cfull = P.hkv * (R.n / kSplitKeys);
-          const int rest = R.n % kSplitKeys;
-          if (rest) cls = 2 + kTilesPerSplit - (rest + kTileKeys - 1) / kTileKeys;
+          // splits before the one holding the first row's window start
+          // hold no visible key and get no item
+          const int lo_min = window_lo(R.n - R.s, P.window);
+          const int kfirst = lo_min / kSplitKeys, nfull = R.n / kSplitKeys;
+          cfull = P.hkv * max(0, nfull - kfirst);
+          if (R.n % kSplitKeys) {
+            // tiles the last split's items run
+            const int t = (R.n + kTileKeys - 1) / kTileKeys -
+                          max(nfull * kTilesPerSplit, lo_min / kTileKeys);
+            cls = 2 + kTilesPerSplit - t;
+          }
         } else if (ncols > kSplitCols) {
           cchunk = (ncols + kChunkCols - 1) / kChunkCols;  // q-tiles per KV head
         }
@@ -305,8 +321,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
   // Pass 2: the split work list.  Wavefront w lists the items of requests
   // w, w + 16, ...: lane j first reads the lengths and offsets of request
   // w + 16 j, then the wavefront takes the requests in turn, its lanes
-  // writing one entry each.  Whole splits of a request are listed
-  // KV-head-major: item off_full + g * nfull + k.
+  // writing one entry each.  Whole splits kfirst .. nfull - 1 of a request
+  // are listed KV-head-major: item off_full + g * (nfull - kfirst) + k - kfirst.
   for (int rb = 0; rb < P.num_seqs; rb += 1024) {
     const int rl = rb + wave + 16 * lane;
     int q0 = 0, s = 0, n = 0, fo = 0, po = -1;  // po < 0: no split items
@@ -317,9 +333,14 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
         s = R.s;
         n = R.n;
         fo = P.off_full[rl];
-        const int rest = R.n % kSplitKeys;
-        po = rest ? pstart[2 + kTilesPerSplit - (rest + kTileKeys - 1) / kTileKeys] + P.off_part[rl]
-                  : 0;
+        if (R.n % kSplitKeys) {
+          const int lo_min = window_lo(R.n - R.s, P.window);
+          const int t = (R.n + kTileKeys - 1) / kTileKeys -
+                        max(R.n / kSplitKeys * kTilesPerSplit, lo_min / kTileKeys);
+          po = pstart[2 + kTilesPerSplit - t] + P.off_part[rl];
+        } else {
+          po = 0;
+        }
       }
     }
     for (int j = 0; j < 64; ++j) {
@@ -333,8 +354,10 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
       R.valid = true;
       const int rfo = __builtin_amdgcn_readlane(fo, j), rpo = __builtin_amdgcn_readlane(po, j);
       const int nfull = R.n / kSplitKeys;
-      for (int idx = lane; idx < P.hkv * nfull; idx += 64)
-        put_item(P, (int64_t)rfo + idx, r, idx / nfull, idx % nfull, R);
+      const int kfirst = window_lo(R.n - R.s, P.window) / kSplitKeys;
+      const int nf = nfull - kfirst;  // whole splits with an item
+      for (int idx = lane; idx < P.hkv * nf; idx += 64)
+        put_item(P, (int64_t)rfo + idx, r, idx / nf, kfirst + idx % nf, R);
       if (R.n % kSplitKeys)
         for (int g = lane; g < P.hkv; g += 64) put_item(P, (int64_t)rpo + g, r, g, nfull, R);
     }
@@ -406,15 +429,16 @@ __device__ __forceinline__ void mask_v(const int64_t (&pb)[kPagesPerTile], int j
 }
 
 // One split item: the tiles of split k of request r, KV head g, for NA
-// column blocks of 16 query-head rows.
-template <int D, int NA>
+// column blocks of 16 query-head rows.  WIN: the handle has a sliding window.
+template <int D, int NA, bool WIN>
 __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k, const Req& R) {
+  const int window = WIN ? P.window : 0;
   const int lane = __lane_id();
   const int col = lane & 15, grp = lane >> 4;
   const int ncols = R.s * P.G;
   const int MS = P.max_splits;
 
-  int pos[NA];
+  int pos[NA], lo[NA];  // visible keys of the column: lo .. pos
   u16x8 qf[NA][D / 32];
   State<D> st[NA];
 #pragma unroll
@@ -422,6 +446,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     const int c = nb * 16 + col;
     const bool v = c < ncols;
     pos[nb] = v ? R.n - R.s + c / P.G : -1;
+    lo[nb] = window_lo(pos[nb], window);
     load_q<D>(P, qf[nb], R.q0 + (v ? c / P.G : 0), g * P.G + (v ? c % P.G : 0), v);
     state_init(st[nb]);
   }
@@ -429,10 +454,15 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
   const int32_t* ptrow = P.pt + (int64_t)r * P.pt_stride;
   const int kt0 = k * kTilesPerSplit;
   const int kt_end = min(kt0 + kTilesPerSplit, (R.n + kTileKeys - 1) / kTileKeys);
+  // the request's first row has the smallest window start: tiles before it
+  // hold no visible key for any column (identity steps), so they are skipped
+  const int lo_min = window_lo(R.n - R.s, window);
+  const int kt_first = max(kt0, lo_min / kTileKeys);
   int64_t pb[kPagesPerTile];
 #pragma unroll
-  for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt0 * kPagesPerTile + b, R.n, g);
-  for (int kt = kt0; kt < kt_end; ++kt) {
+  for (int b = 0; b < kPagesPerTile; ++b)
+    pb[b] = page_block(P, ptrow, kt_first * kPagesPerTile + b, R.n, g);
+  for (int kt = kt_first; kt < kt_end; ++kt) {
     const int j0 = kt * kTileKeys;
     const bool full = j0 + kTileKeys <= R.n && pb[0] >= 0 && pb[1] >= 0 && pb[2] >= 0 && pb[3] >= 0;
     u16x8 kf[kPagesPerTile][D / 32];
@@ -453,13 +483,16 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     TileWeights w[NA];
     bool open = true;  // every key of the tile visible to every column
 #pragma unroll
-    for (int nb = 0; nb < NA; ++nb) open = open && __all(pos[nb] >= j0 + kTileKeys - 1);
+    for (int nb = 0; nb < NA; ++nb)
+      open = open && __all(pos[nb] >= j0 + kTileKeys - 1 && lo[nb] <= j0);
     if (open) {
 #pragma unroll
-      for (int nb = 0; nb < NA; ++nb) w[nb] = tile_softmax<D, false>(st[nb], acc[nb], j0, pos[nb], P.c);
+      for (int nb = 0; nb < NA; ++nb)
+        w[nb] = tile_softmax<D, false, WIN>(st[nb], acc[nb], j0, pos[nb], lo[nb], P.c);
     } else {
 #pragma unroll
-      for (int nb = 0; nb < NA; ++nb) w[nb] = tile_softmax<D, true>(st[nb], acc[nb], j0, pos[nb], P.c);
+      for (int nb = 0; nb < NA; ++nb)
+        w[nb] = tile_softmax<D, true, WIN>(st[nb], acc[nb], j0, pos[nb], lo[nb], P.c);
     }
 #pragma unroll
     for (int m = 0; m < D / 16; ++m) {
@@ -471,8 +504,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     for (int nb = 0; nb < NA; ++nb) tile_commit<D>(st[nb], w[nb]);
   }
 
-  const int nsplit = (R.n - 1) / kSplitKeys + 1;
-  if (nsplit == 1) {
+  if (request_splits(R, window) == 1) {
     // a single split: the merged state is this state; normalise and store
 #pragma unroll
     for (int nb = 0; nb < NA; ++nb) {
@@ -482,11 +514,11 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     }
     return;
   }
-  // partial state of split k for every column that has a key in it
+  // partial state of split k for every column that has a visible key in it
 #pragma unroll
   for (int nb = 0; nb < NA; ++nb) {
     const int c = nb * 16 + col;
-    if (pos[nb] < 0 || k > pos[nb] / kSplitKeys) continue;
+    if (pos[nb] < 0 || k > pos[nb] / kSplitKeys || k < lo[nb] / kSplitKeys) continue;
     const int64_t pidx = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS + k;
     if (grp == 0) {
       P.ws_m[pidx] = st[nb].m;
@@ -500,7 +532,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 
 // One wavefront per workgroup: a finished item frees its slot at once, which
 // keeps the end of the launch short when item durations vary.
-template <int D, int NB>
+template <int D, int NB, bool WIN>
 __global__ __launch_bounds__(64) void split_kernel(Params P) {
   // the item's work-list entry: all 8 words in one scalar load, so that the
   // exit test and the item's fields cost a single round trip (the list is
@@ -520,9 +552,9 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
   R.valid = true;
   // column blocks actually used by this request: one wave-uniform dispatch
   if (NB == 2 && R.s * P.G > 16)
-    split_item<D, NB>(P, r, g, k, R);
+    split_item<D, NB, WIN>(P, r, g, k, R);
   else
-    split_item<D, 1>(P, r, g, k, R);
+    split_item<D, 1, WIN>(P, r, g, k, R);
 }
 
 // Contexts of up to this many splits are merged by the short merge kernel.
@@ -546,10 +578,13 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   if (!R.valid) return;
   const int ncols = R.s * P.G;
   if (ncols > P.split_cols || c >= ncols) return;
-  if ((R.n - 1) / kSplitKeys == 0) return;  // one split: written by the split kernel
+  if (request_splits(R, P.window) == 1) return;  // written by the split kernel
   const int MS = P.max_splits;
-  const int kp = (R.n - R.s + c / P.G) / kSplitKeys + 1;
-  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS;
+  // the row's splits: from the one holding its window start through its own
+  const int pr = R.n - R.s + c / P.G;
+  const int klo = window_lo(pr, P.window) / kSplitKeys;
+  const int kp = pr / kSplitKeys + 1 - klo;
+  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS + klo;
   // every partial state is loaded first (at most kShortMerge of them), then
   // folded in ascending split order
   float mk[kShortMerge], zk[kShortMerge];
@@ -603,7 +638,7 @@ __global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
   if (!R.valid) return;
   const int ncols = R.s * P.G;
   if (ncols > P.split_cols) return;
-  const int nsplit = (R.n - 1) / kSplitKeys + 1;
+  const int nsplit = request_splits(R, P.window);  // bounds every row's split count
   if (nsplit == 1) return;  // written by the split kernel
   const int e0 = slice * 256;
   if (e0 >= ncols * D) return;
@@ -617,15 +652,20 @@ __global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
   const bool mine = e < ncols * D;
   const int c = mine ? e / D : cfirst;
   const int d = e % D;
-  const int kp = (R.n - R.s + c / P.G) / kSplitKeys + 1;
-  const int64_t pu = (base + (int64_t)c * MS) * D + d;
+  // row c's splits: from the one holding its window start through its own
+  const int pr = R.n - R.s + c / P.G;
+  const int klo = window_lo(pr, P.window) / kSplitKeys;
+  const int kp = pr / kSplitKeys + 1 - klo;
+  const int64_t pu = (base + (int64_t)c * MS + klo) * D + d;
   float W = 0.f;
   for (int k0 = 0; k0 < nsplit; k0 += CH) {
     // per-column factors of this chunk: wavefront w takes columns w, w + 4, ...
     for (int ci = wave; ci < ncs; ci += 4) {
       const int cc = cfirst + ci;
-      const int kpc = (R.n - R.s + cc / P.G) / kSplitKeys + 1;
-      const int64_t p0 = base + (int64_t)cc * MS;
+      const int pc = R.n - R.s + cc / P.G;
+      const int kloc = window_lo(pc, P.window) / kSplitKeys;
+      const int kpc = pc / kSplitKeys + 1 - kloc;
+      const int64_t p0 = base + (int64_t)cc * MS + kloc;
       const int k = k0 + lane;
       const bool has = k < kpc;
       const float mk = has ? P.ws_m[p0 + k] : -__builtin_inff();
@@ -721,10 +761,12 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int D>
 // Two workgroups per CU (waves_per_eu 2: at most 256 registers per lane, and
 // two LDS rings of kChunkStages tiles): while one wavefront of a SIMD waits on
-// its softmax chain, the other issues matrix-core work.
+// its softmax chain, the other issues matrix-core work.  WIN: the handle has a
+// sliding window; without one every window term is the constant 0 and
+// compiles away (the kernel is at its register budget).
+template <int D, bool WIN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void chunk_kernel(Params P) {
   constexpr int NB = 2;
   constexpr int BLK = kPage * D;                   // elements of one page block
@@ -736,6 +778,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int wave = uni(threadIdx.x >> 6);
   const int lane = __lane_id();
   const int col = lane & 15;
+  const int window = WIN ? P.window : 0;
   // Items are ordered (KV head, request, q-tile) and blocks of one XCD (block
   // id mod 8) take a contiguous range of them: the q-tiles of one (request,
   // KV head) share that XCD's L2, and with 8 KV heads each XCD takes one head
@@ -757,7 +800,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int cend = min(ncols, c0 + kChunkCols);
   const int pmax = R.n - R.s + (cend - 1) / P.G;  // last position of the block
 
-  int pos[NB];
+  int pos[NB], lo[NB];  // visible keys of the column: lo .. pos
   u16x8 qf[NB][D / 32];
   State<D> st[NB];
   float M[NB], Z[NB];
@@ -768,6 +811,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int c = c0 + wave * 32 + nb * 16 + col;
     const bool v = c < cend;
     pos[nb] = v ? R.n - R.s + c / P.G : -1;
+    lo[nb] = window_lo(pos[nb], window);
     load_q<D>(P, qf[nb], R.q0 + (v ? c / P.G : 0), g * P.G + (v ? c % P.G : 0), v);
     const int cb = c0 + wave * 32 + nb * 16;
     const int clast = min(cend, cb + 16) - 1;
@@ -780,6 +824,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   const int32_t* ptrow = P.pt + (int64_t)r * P.pt_stride;
   const int ntiles = pmax / kTileKeys + 1;
+  // the block's first row has the smallest window start: earlier tiles hold
+  // no visible key for any column of the block (identity steps)
+  const int kt_first = window_lo(R.n - R.s + c0 / P.G, window) / kTileKeys;
+  // this wavefront's smallest window start (its first valid column)
+  const int wave_lo = window_lo(R.n - R.s + min(c0 + wave * 32, cend - 1) / P.G, window);
   // Issues this wavefront's WCH direct loads of tile kt into stage buf: copy
   // q = wave * WCH + w moves 1 KB of page block q / (BLK / 512).
   auto fetch = [&](int kt, int buf) {
@@ -835,8 +884,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   wait_vmcnt<0>();  // the Q operands are in registers before any tile copy is issued
 #pragma unroll
   for (int t = 0; t < STAGES - 1; ++t)
-    if (t < ntiles) fetch(t, t);
-  for (int kt = 0; kt < ntiles; ++kt) {
+    if (kt_first + t < ntiles) fetch(kt_first + t, (kt_first + t) % STAGES);
+  for (int kt = kt_first; kt < ntiles; ++kt) {
     const int j0 = kt * kTileKeys;
     const int k = kt / kTilesPerSplit;
     const int buf = kt % STAGES;
@@ -857,12 +906,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       lds_barrier();
     }
     if (kt + STAGES - 1 < ntiles) fetch(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    if (kt % kTilesPerSplit == 0) {
+    if (kt % kTilesPerSplit == 0 || kt == kt_first) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) state_init(st[nb]);
     }
     const uint16_t* T = lds + buf * NBLK * BLK;
-    if (wave_pmax >= j0) {
+    if (wave_pmax >= j0 && j0 + kTileKeys - 1 >= wave_lo) {
       f32x4 acc[NB][kPagesPerTile];
       tile_scores<D, NB>(
           [&](int b, int ks) { return *reinterpret_cast<const u16x8*>(T + b * BLK + 512 * ks + 8 * lane); },
@@ -870,13 +919,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       TileWeights w[NB];
       bool open = true;  // every key of the tile visible to every column
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) open = open && __all(pos[nb] >= j0 + kTileKeys - 1);
+      for (int nb = 0; nb < NB; ++nb)
+        open = open && __all(pos[nb] >= j0 + kTileKeys - 1 && lo[nb] <= j0);
       if (open) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D, false>(st[nb], acc[nb], j0, pos[nb], P.c);
+        for (int nb = 0; nb < NB; ++nb)
+          w[nb] = tile_softmax<D, false, WIN>(st[nb], acc[nb], j0, pos[nb], lo[nb], P.c);
       } else {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D, true>(st[nb], acc[nb], j0, pos[nb], P.c);
+        for (int nb = 0; nb < NB; ++nb)
+          w[nb] = tile_softmax<D, true, WIN>(st[nb], acc[nb], j0, pos[nb], lo[nb], P.c);
       }
 #pragma unroll
       for (int m = 0; m < D / 16; ++m) {
@@ -895,8 +947,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       // split k ends: fold it into the running merge for columns that have it
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        if (pos[nb] < 0 || k > pos[nb] / kSplitKeys) continue;
-        if (k == 0) {
+        // the column's splits run from the one holding its window start
+        const int klo = lo[nb] / kSplitKeys;
+        if (pos[nb] < 0 || k > pos[nb] / kSplitKeys || k < klo) continue;
+        if (k == klo) {
           M[nb] = st[nb].m;
           Z[nb] = st[nb].z;
 #pragma unroll
@@ -946,6 +1000,7 @@ __global__ __launch_bounds__(256) void kv_write_kernel(const uint16_t* knew, con
 // ---------------------------------------------------------------------------
 struct vd_attn {
   int32_t hq, hkv, d, page_size, group;
+  int32_t window;  // sliding window in keys, 0 = none
   float scale;
   float c;  // scale * log2(e) in fp32
 };
@@ -1024,6 +1079,7 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.hq = h->hq;
   P.hkv = h->hkv;
   P.G = h->group;
+  P.window = h->window;
   P.c = h->c;
   const bool writes = b->k_new && b->num_new_tokens > 0;
   P.knew = writes ? static_cast<const uint16_t*>(b->k_new) : nullptr;
@@ -1054,10 +1110,11 @@ int run_splits(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent
   const int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
   if (items > INT32_MAX - 4) return VD_ERR_INVALID_ARG;
   const dim3 grid((unsigned)items), block(64);
-  if (P.split_cols == 16)
-    hipExtLaunchKernelGGL((split_kernel<D, 1>), grid, block, 0, s, e0, e1, 0, P);
-  else
-    hipExtLaunchKernelGGL((split_kernel<D, 2>), grid, block, 0, s, e0, e1, 0, P);
+  // a handle's window is fixed at creation: one kernel per handle and width
+  const bool win = P.window > 0;
+  const auto kern = P.split_cols == 16 ? (win ? &split_kernel<D, 1, true> : &split_kernel<D, 1, false>)
+                                       : (win ? &split_kernel<D, 2, true> : &split_kernel<D, 2, false>);
+  hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, P);
   return launched();
 }
 
@@ -1087,12 +1144,16 @@ int run_chunks(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent
   blocks = (blocks + 7) / 8 * 8;
   if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
   constexpr size_t lds = chunk_lds_bytes<D>();
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&chunk_kernel<D>), hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)lds);
-  if (attr != hipSuccess) return VD_ERR_LAUNCH;
-  hipExtLaunchKernelGGL((chunk_kernel<D>), dim3((unsigned)blocks), dim3(256), (uint32_t)lds, s, e0,
-                        e1, 0, P);
+  // a handle's window is fixed at creation: one kernel per handle
+  const auto kern = P.window > 0 ? &chunk_kernel<D, true> : &chunk_kernel<D, false>;
+  static const hipError_t attr0 = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&chunk_kernel<D, false>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static const hipError_t attr1 = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&chunk_kernel<D, true>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr0 != hipSuccess || attr1 != hipSuccess) return VD_ERR_LAUNCH;
+  hipExtLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), (uint32_t)lds, s, e0, e1, 0, P);
   return launched();
 }
 
@@ -1116,6 +1177,7 @@ int vd_attn_create(const vd_attn_desc* desc, vd_attn** out) {
       desc->page_size < 1)
     return VD_ERR_INVALID_ARG;
   if (!(desc->softmax_scale == desc->softmax_scale)) return VD_ERR_INVALID_ARG;  // NaN
+  if (desc->window < 0) return VD_ERR_INVALID_ARG;
   if (desc->dtype != VD_DTYPE_BF16) return VD_ERR_UNSUPPORTED;
   if (desc->head_dim != 64 && desc->head_dim != 128) return VD_ERR_UNSUPPORTED;
   if (desc->page_size != kPage) return VD_ERR_UNSUPPORTED;
@@ -1128,6 +1190,7 @@ int vd_attn_create(const vd_attn_desc* desc, vd_attn** out) {
   h->d = desc->head_dim;
   h->page_size = desc->page_size;
   h->group = desc->num_q_heads / desc->num_kv_heads;
+  h->window = desc->window;
   const double scale = desc->softmax_scale > 0.0f ? (double)desc->softmax_scale
                                                   : 1.0 / std::sqrt((double)desc->head_dim);
   h->scale = (float)scale;

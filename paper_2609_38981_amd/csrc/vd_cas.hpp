@@ -118,9 +118,17 @@ __device__ __forceinline__ void tile_scores(const KF& kf, const u16x8 (&qf)[NB][
     }
 }
 
+// First key visible to position p: 0, or with a sliding window of w > 0
+// keys (Appendix A.5) the window's start, so that key j is visible when
+// lo <= j <= p.
+__device__ __forceinline__ int window_lo(int p, int w) {
+  return (w > 0 && p - w + 1 > 0) ? p - w + 1 : 0;
+}
+
 // Softmax half of Appendix A.2's update for the tile starting at logical key
-// j0, for the column at position p (p < 0: a padding column, never visible);
-// c is the base-two scale applied to the raw dot.  Produces the weights (cast
+// j0, for the column at position p whose visible keys are lo..p (p < 0: a
+// padding column, never visible); c is the base-two scale applied to the raw
+// dot.  Produces the weights (cast
 // to bf16, the cache type, as the B operand of P.V), alpha, and the candidate
 // (m, z); h says whether the column sees any key of the tile.
 struct TileWeights {
@@ -131,12 +139,14 @@ struct TileWeights {
 
 //
 // MASKED = false may be used only when every key of the tile is visible to
-// every column of the wavefront (p >= j0 + 63 in all lanes): all selects
-// then take their first operand, so both forms give the same bits.
-template <int D, bool MASKED = true>
+// every column of the wavefront (lo <= j0 and p >= j0 + 63 in all lanes): all
+// selects then take their first operand, so both forms give the same bits.
+// WIN = false may be used only when lo = 0 (no sliding window): the test
+// key >= lo is then always true and is left out.
+template <int D, bool MASKED = true, bool WIN = true>
 __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
                                                     const f32x4 (&acc)[kPagesPerTile], int j0,
-                                                    int p, float c) {
+                                                    int p, int lo, float c) {
   const int grp = __lane_id() >> 4;
   float g[kPagesPerTile][4];
   bool lam[kPagesPerTile][4];
@@ -145,7 +155,7 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int key = j0 + 16 * b + 4 * grp + i;
-      lam[b][i] = !MASKED || key <= p;
+      lam[b][i] = !MASKED || (key <= p && (!WIN || key >= lo));
       g[b][i] = acc[b][i] * c;
     }
   // masked maximum over the tile: fixed tree in the lane, then lanes ^16, ^32
@@ -162,7 +172,7 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
   mx = fmax_(mx, xor_lane(mx, 16));
   mx = fmax_(mx, xor_lane(mx, 32));
   TileWeights w;
-  w.h = !MASKED || j0 <= p;  // any visible key in this tile for this column
+  w.h = !MASKED || (j0 <= p && (!WIN || j0 + kTileKeys - 1 >= lo));  // any visible key
   w.m_new = fmax_(st.m, mx);
   // A column with no visible key keeps its state (tile_commit), and its
   // operands are zeroed so that nothing non-finite enters the matrix core.

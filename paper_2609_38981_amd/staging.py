@@ -35,7 +35,8 @@ class DeviceCall:
 
 
 def handle_for(shape: W.Shape) -> VdAttn:
-    return VdAttn(shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.page_size)
+    return VdAttn(shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.page_size,
+                  window=shape.window)
 
 
 def fill_pool(attn: VdAttn, call: W.Call, k_pool: torch.Tensor, v_pool: torch.Tensor,

@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(HERE, "libvdattn.so")
 HEADER = os.path.join(ROOT, "include", "vdattn.h")
 
 VD_OK = 0
-VD_ABI_VERSION = 1
+VD_ABI_VERSION = 2
 VD_DTYPE_BF16 = 1
 TILE_KEYS = 64
 SPLIT_KEYS = 512
@@ -41,7 +41,7 @@ class _Desc(ctypes.Structure):
     _fields_ = [("abi_version", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float), ("window", ctypes.c_int32)]
 
 
 class _Batch(ctypes.Structure):
@@ -156,15 +156,16 @@ class VdAttn:
     """Handle of one fixed attention configuration (immutable)."""
 
     def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, page_size: int = 16,
-                 softmax_scale: float = 0.0):
+                 softmax_scale: float = 0.0, window: int = 0):
         self.lib = load_library()
         d = _Desc(VD_ABI_VERSION, num_q_heads, num_kv_heads, head_dim, page_size, VD_DTYPE_BF16,
-                  float(softmax_scale))
+                  float(softmax_scale), int(window))
         h = ctypes.c_void_p()
         _check(self.lib.vd_attn_create(ctypes.byref(d), ctypes.byref(h)), "vd_attn_create")
         self._h = h
         self.num_q_heads, self.num_kv_heads, self.head_dim = num_q_heads, num_kv_heads, head_dim
         self.page_size = page_size
+        self.window = int(window)
         self.softmax_scale = softmax_scale if softmax_scale > 0 else 1.0 / math.sqrt(head_dim)
 
     def __del__(self):

@@ -95,6 +95,7 @@ class Shape:
     num_kv_heads: int
     head_dim: int
     page_size: int = 16
+    window: int = 0  # sliding-window attention span in keys; 0 = full causal prefix
 
     @property
     def group(self) -> int:
@@ -104,6 +105,8 @@ class Shape:
 TINY = Shape(4, 2, 64)
 LLAMA8B = Shape(32, 8, 128)
 LLAMA70B = Shape(64, 8, 128)
+# Llama-3-8B head geometry with a 4096-key sliding window (Appendix A.5)
+LLAMA8B_SWA4K = Shape(32, 8, 128, window=4096)
 
 
 # ---------------------------------------------------------------------------
@@ -236,25 +239,35 @@ class Call:
         return int(np.searchsorted(cu, row, side="right") - 1)
 
     # -- pool contents ------------------------------------------------------
+    def first_key(self, ri: int) -> int:
+        """First key any row of request ri can see: 0, or with a sliding
+        window of w keys the window start of its first row, max(0, n - s - w + 1)."""
+        r, w = self.reqs[ri], self.shape.window
+        return max(0, r.n - r.s - w + 1) if w > 0 else 0
+
     def kv_bytes(self) -> int:
-        """Algorithmic K+V bytes: every request reads its n keys once."""
+        """Algorithmic K+V bytes: every request reads each key its rows can see
+        (keys first_key .. n - 1) once."""
         sh = self.shape
-        return int(sum(r.n for r in self.reqs)) * sh.num_kv_heads * sh.head_dim * 2 * 2
+        keys = sum(r.n - self.first_key(ri) for ri, r in enumerate(self.reqs))
+        return int(keys) * sh.num_kv_heads * sh.head_dim * 2 * 2
 
     def unique_kv_bytes(self, req_indices=None) -> int:
         """K+V bytes of the distinct cache slots the given requests (default:
-        all) read: a page shared by several requests counts once, with the
-        largest number of its slots any of them reads."""
+        all) read (the keys their rows can see): a slot of a page shared by
+        several requests counts once."""
         sh = self.shape
         P = sh.page_size
         idx = range(len(self.reqs)) if req_indices is None else req_indices
-        used = {}
+        used = {}  # page -> bit mask of its slots read
         for ri in idx:
-            n = int(self.context_lens[ri])
-            for lp in range(-(-n // P)):
+            n, lo = int(self.context_lens[ri]), self.first_key(ri)
+            for lp in range(lo // P, -(-n // P)):
                 page = int(self.page_table[ri, lp])
-                used[page] = max(used.get(page, 0), min(P, n - lp * P))
-        return int(sum(used.values())) * sh.num_kv_heads * sh.head_dim * 2 * 2
+                a, b = max(0, lo - lp * P), min(P, n - lp * P)
+                used[page] = used.get(page, 0) | (((1 << (b - a)) - 1) << a)
+        slots = sum(bin(m).count("1") for m in used.values())
+        return int(slots) * sh.num_kv_heads * sh.head_dim * 2 * 2
 
     def new_tokens(self) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
         """This call's own tokens (positions n - s .. n - 1 of every request):

@@ -84,7 +84,7 @@ def oracle_run(call: W.Call, rows=None) -> np.ndarray:
     return oracle.paged_attention(call.q_bits(), call.cu_q_lens, call.context_lens,
                                   call.page_table, kp, vp, num_q_heads=sh.num_q_heads,
                                   num_kv_heads=sh.num_kv_heads, head_dim=sh.head_dim,
-                                  page_size=sh.page_size, rows=rows)
+                                  page_size=sh.page_size, window=sh.window, rows=rows)
 
 
 def by_position(call: W.Call, out: np.ndarray):

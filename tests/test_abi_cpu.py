@@ -23,8 +23,8 @@ def test_exports_every_declared_function(lib):
 
 
 def _create(lib, **kw):
-    d = dict(abi_version=1, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16, dtype=1,
-             softmax_scale=0.0)
+    d = dict(abi_version=V.VD_ABI_VERSION, num_q_heads=32, num_kv_heads=8, head_dim=128,
+             page_size=16, dtype=1, softmax_scale=0.0, window=0)
     d.update(kw)
     desc = V._Desc(**d)
     h = ctypes.c_void_p()
@@ -33,8 +33,9 @@ def _create(lib, **kw):
 
 
 def test_create_supported_and_destroy(lib):
-    for hq, hkv, d in [(32, 8, 128), (64, 8, 128), (4, 2, 64), (8, 8, 64)]:
-        rc, h = _create(lib, num_q_heads=hq, num_kv_heads=hkv, head_dim=d)
+    for hq, hkv, d, w in [(32, 8, 128, 0), (64, 8, 128, 0), (4, 2, 64, 0), (8, 8, 64, 0),
+                          (32, 8, 128, 4096), (4, 2, 64, 1)]:
+        rc, h = _create(lib, num_q_heads=hq, num_kv_heads=hkv, head_dim=d, window=w)
         assert rc == 0 and h.value
         a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
         assert lib.vd_attn_tiling(h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == 0
@@ -46,8 +47,9 @@ def test_create_supported_and_destroy(lib):
 @pytest.mark.parametrize("kw,code", [
     (dict(head_dim=96), -2), (dict(head_dim=256), -2), (dict(page_size=32), -2),
     (dict(dtype=2), -2), (dict(num_q_heads=12, num_kv_heads=8), -2),
-    (dict(num_q_heads=64, num_kv_heads=1), -2), (dict(abi_version=2), -1),
-    (dict(num_kv_heads=0), -1), (dict(softmax_scale=float("nan")), -1),
+    (dict(num_q_heads=64, num_kv_heads=1), -2), (dict(abi_version=3), -1),
+    (dict(num_kv_heads=0), -1), (dict(softmax_scale=float("nan")), -1), (dict(window=-1), -1),
+    (dict(abi_version=1), -1),
 ])
 def test_create_rejects(lib, kw, code):
     rc, h = _create(lib, **kw)
