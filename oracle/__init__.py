@@ -58,7 +58,7 @@ def bind(path: str):
     lib.vdo_paged_attention.argtypes = [
         ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
         ctypes.c_int, ctypes.c_double, ctypes.c_int, P, P, P, P, ctypes.c_int, P, P,
-        ctypes.c_int64, P, P, ctypes.c_int]
+        ctypes.c_int64, P, P, P, ctypes.c_int]
     lib.vdo_default_threads.restype = ctypes.c_int
     return lib
 
@@ -83,7 +83,7 @@ def _c(a, dtype):
 
 def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_pool_bits,
                     *, num_q_heads, num_kv_heads, head_dim, page_size, scale=None,
-                    window=0, rows=None, threads=0, lib=None) -> np.ndarray:
+                    window=0, rows=None, threads=0, lib=None, with_lse=False):
     """Exact (fp64) paged causal attention.
 
     q_bits:        uint16 [T, Hq, D] bf16 bit patterns, rows packed by request.
@@ -98,8 +98,10 @@ def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_
                    those rows are computed, the rest of the result is NaN.
     threads:       host threads (0 = all online cores).
     lib:           an alternative library from ``bind`` (tests of the pins).
+    with_lse:      also return the rows' log-sum-exp of the scaled scores over
+                   the visible keys (natural log), float64 [T, Hq].
 
-    Returns float64 [T, Hq, D].
+    Returns float64 [T, Hq, D] (and the log-sum-exp with ``with_lse``).
     """
     lib = _load() if lib is None else lib
     q_bits, qp = _c(q_bits, np.uint16)
@@ -129,11 +131,13 @@ def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_
             sel[rows_arr.astype(np.int64)] = 1
         sel, selp = _c(sel, np.uint8)
     out = np.full((T, num_q_heads, head_dim), np.nan, np.float64)
+    lse = np.full((T, num_q_heads), np.nan, np.float64) if with_lse else None
     rc = lib.vdo_paged_attention(
         B, T, num_q_heads, num_kv_heads, head_dim, page_size, float(scale), int(window), qp,
         cup, ctxp, ptp, stride, kpp, vpp, kp.shape[0], selp,
-        out.ctypes.data_as(ctypes.c_void_p), int(threads))
+        out.ctypes.data_as(ctypes.c_void_p),
+        lse.ctypes.data_as(ctypes.c_void_p) if with_lse else None, int(threads))
     if rc != 0:
         raise ValueError("oracle rejected the call: %s (%d)" % (ERRORS.get(rc, "?"), rc))
-    return out
+    return (out, lse) if with_lse else out
 

@@ -28,6 +28,11 @@
  *   which is exactly softmax attention restricted to the causal prefix
  *   j <= p (the mask of Appendix A.2 reduces to j <= p because p < n).
  *
+ *   Optionally also the row's log-sum-exp (the normaliser the paper's tile
+ *   update carries as (m, z), Appendix A.2; the paper does not export it):
+ *       lse = log sum_j exp(score_j) = max_j score_j + log sum_j exp(score_j - max)
+ *   in natural log, over the same visible keys.
+ *
  *   Sliding-window attention (Appendix A.5, "Relational Alignment and
  *   Composition"): with a window size w > 0 shared by the call, key j is
  *   visible to position p only when also j > p - w, so the sums above run
@@ -74,6 +79,7 @@ typedef struct {
   int64_t num_pages;
   const uint8_t *row_select;
   double *out;
+  double *lse; /* optional [T, Hq] */
   /* work queue over (request, q-head) pairs */
   int64_t next_item;
   pthread_mutex_t lock;
@@ -117,6 +123,7 @@ static int run_item(job_t *J, int r, int h, double *score, double *w) {
       denom += w[j];
     }
     for (int j = lo; j <= p; ++j) w[j] /= denom;
+    if (J->lse) J->lse[t * J->hq + h] = mx + log(denom);
     /* weighted sum of values */
     double *orow = J->out + (t * J->hq + h) * (int64_t)D;
     for (int dd = 0; dd < D; ++dd) orow[dd] = 0.0;
@@ -177,7 +184,8 @@ static int validate(const job_t *J) {
   return VDO_OK;
 }
 
-/* window: 0 for the full causal prefix, w > 0 for a sliding window of w keys */
+/* window: 0 for the full causal prefix, w > 0 for a sliding window of w keys;
+ * lse: optional [T, Hq] output of the rows' log-sum-exp (NULL: not written) */
 int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
                         int num_kv_heads, int head_dim, int page_size,
                         double scale, int window, const uint16_t *q,
@@ -185,7 +193,7 @@ int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
                         const int32_t *page_table, int pt_stride,
                         const uint16_t *k_pool, const uint16_t *v_pool,
                         int64_t num_pages, const uint8_t *row_select,
-                        double *out, int num_threads) {
+                        double *out, double *lse, int num_threads) {
   if (!q || !cu_q_lens || !context_lens || !page_table || !k_pool || !v_pool ||
       !out)
     return VDO_ERR_ARG;
@@ -209,6 +217,7 @@ int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
   J.num_pages = num_pages;
   J.row_select = row_select;
   J.out = out;
+  J.lse = lse;
   int rc = validate(&J);
   if (rc != VDO_OK) return rc;
 

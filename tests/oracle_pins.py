@@ -8,6 +8,8 @@ disagrees with the fact it is pinned to:
   float64 (causal prefill, a chunk at a key offset via an explicit ``tril``
   mask, grouped-query heads via ``enable_gqa``, a sliding window via a banded
   mask), and ``scipy.special.softmax``;
+* the log-sum-exp output: scipy's ``logsumexp``; log(count) for a zero query,
+  the score of a single key, weights exp(score - lse) summing to one;
 * closed forms: a single visible key (n = 1, row 0, or a window of 1) returns
   that key's value exactly; a zero query or identical keys give the plain mean
   of the visible values (the prefix, or the window); one dominant score
@@ -68,10 +70,11 @@ def pack(reqs, hq, hkv, d, P, num_pages=None, rng=None, pages=None, poison=True)
     return q, cu, ctx, pt, kp, vp
 
 
-def run(lib, reqs, hq, hkv, d, P, scale=None, window=0, **kw):
+def run(lib, reqs, hq, hkv, d, P, scale=None, window=0, with_lse=False, **kw):
     q, cu, ctx, pt, kp, vp = pack(reqs, hq, hkv, d, P, **kw)
     return oracle.paged_attention(q, cu, ctx, pt, kp, vp, num_q_heads=hq, num_kv_heads=hkv,
-                                  head_dim=d, page_size=P, scale=scale, window=window, lib=lib)
+                                  head_dim=d, page_size=P, scale=scale, window=window, lib=lib,
+                                  with_lse=with_lse)
 
 
 def rand_req(rng, s, n, hq, hkv, d):
@@ -322,10 +325,59 @@ def pin_window_limits(lib):
     assert not np.array_equal(a[0], c[0])
 
 
+# -- log-sum-exp of the visible scaled scores (natural log) ---------------------
+def pin_lse_scipy(lib):
+    """Dense brute force with scipy's logsumexp on tiny requests, with and
+    without a window."""
+    rng = np.random.default_rng(31)
+    hq, hkv, d, P = 2, 1, 8, 2
+    s, n = 4, 11
+    req = rand_req(rng, s, n, hq, hkv, d)
+    for w in (0, 3):
+        _, lse = run(lib, [req], hq, hkv, d, P, window=w, with_lse=True)
+        q, k = f64(req["q"]), f64(req["k"])
+        for i in range(s):
+            p = n - s + i
+            lo = max(0, p - w + 1) if w else 0
+            for h in range(hq):
+                sc = (k[lo:p + 1, 0, :] @ q[i, h]) / np.sqrt(d)
+                np.testing.assert_allclose(lse[i, h], scipy.special.logsumexp(sc), rtol=0,
+                                           atol=1e-12)
+
+
+def pin_lse_closed_forms(lib):
+    """q = 0 gives lse = log(number of visible keys); one visible key gives
+    its own score; and the weights exp(score - lse) sum to one."""
+    rng = np.random.default_rng(32)
+    hq, hkv, d, P = 4, 2, 16, 4
+    req = rand_req(rng, 5, 23, hq, hkv, d)
+    zq = {k: v.copy() for k, v in req.items()}
+    zq["q"][:] = 0
+    for w in (0, 7):
+        _, lse = run(lib, [zq], hq, hkv, d, P, window=w, with_lse=True)
+        for i in range(5):
+            p = 18 + i
+            cnt = min(p + 1, w) if w else p + 1
+            assert np.all(lse[i] == np.log(cnt)), (w, i)
+    one = rand_req(rng, 1, 1, hq, hkv, d)
+    _, lse = run(lib, [one], hq, hkv, d, P, with_lse=True)
+    q, k = f64(one["q"]), f64(one["k"])
+    for h in range(hq):
+        np.testing.assert_allclose(lse[0, h], (q[0, h] @ k[0, h // 2]) / np.sqrt(d), rtol=0,
+                                   atol=1e-12)
+    _, lse = run(lib, [req], hq, hkv, d, P, with_lse=True)
+    q, k = f64(req["q"]), f64(req["k"])
+    for i in range(5):
+        p = 18 + i
+        for h in range(hq):
+            sc = (k[:p + 1, h // 2, :] @ q[i, h]) / np.sqrt(d)
+            np.testing.assert_allclose(np.exp(sc - lse[i, h]).sum(), 1.0, rtol=0, atol=1e-12)
+
+
 ALL_PINS = [pin_sdpa_prefill, pin_sdpa_chunk_offset, pin_sdpa_scale, pin_scipy_softmax_dense,
             pin_single_key, pin_zero_query_mean, pin_identical_keys_mean, pin_dominant_key,
             pin_fig4_example, pin_invariances, pin_sdpa_window, pin_window_one_key,
-            pin_window_zero_query_mean, pin_window_limits]
+            pin_window_zero_query_mean, pin_window_limits, pin_lse_scipy, pin_lse_closed_forms]
 
 
 if __name__ == "__main__":

@@ -103,6 +103,9 @@ MUTANTS = {
     "window_off_by_one": ("p - J->window + 1 > 0) ? p - J->window + 1 : 0;",
                           "p - J->window > 0) ? p - J->window : 0;"),
     "window_ignored": ("const int lo = (J->window > 0 &&", "const int lo = (J->window < 0 &&"),
+    "lse_log2": ("J->lse[t * J->hq + h] = mx + log(denom);", "J->lse[t * J->hq + h] = mx + log2(denom);"),
+    "lse_no_max": ("J->lse[t * J->hq + h] = mx + log(denom);", "J->lse[t * J->hq + h] = log(denom);"),
+    "lse_sign": ("J->lse[t * J->hq + h] = mx + log(denom);", "J->lse[t * J->hq + h] = mx - log(denom);"),
     "window_from_n": ("p - J->window + 1 > 0) ? p - J->window + 1 : 0;",
                       "n - J->window + 1 > 0) ? n - J->window + 1 : 0;"),
 }
