@@ -169,13 +169,13 @@ def main():
         ws = attn.new_workspace(call.num_seqs, dc.batch.max_q_len, dc.batch.max_context_len)
         reps.append((dc, ws, torch.empty_like(dc.batch.q)))
     P = sh.page_size
-    # this step's new tokens (positions n - s .. n - 1 of every request): the
-    # plan phase writes them into the pool before attention reads it
-    kn, vn, sl = call.new_tokens()
+    # this step's new tokens (the K/V of the query rows, positions n - s .. n - 1
+    # of every request): the call writes them into the pool before attention
+    # reads it (the split items themselves, or the plan launch)
+    kn, vn = call.query_kv()
     k_new, v_new = S.bf16_tensor(kn, "cuda"), S.bf16_tensor(vn, "cuda")
-    slot_t = torch.from_numpy(sl).cuda()
     for dc, _, _ in reps:
-        dc.batch.k_new, dc.batch.v_new, dc.batch.slot_mapping = k_new, v_new, slot_t
+        dc.batch.k_new, dc.batch.v_new = k_new, v_new
     torch.cuda.synchronize()
     log("staged %d replicas" % len(reps))
 

@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define VD_ABI_VERSION 2
+#define VD_ABI_VERSION 3
 
 typedef enum {
   VD_OK = 0,
@@ -112,39 +112,51 @@ typedef struct {
   int64_t num_pages;            /* >= 1 */
   int32_t max_q_len;            /* HOST hint: >= every s_r (launch sizing only) */
   int32_t max_context_len;      /* HOST hint: >= every n_r (launch sizing only) */
-  /* Optional: this call's new tokens, written into the pool by the plan phase
-   * before any attention kernel reads it (append + attend in one call; the
-   * same arguments and layout as vd_kv_write).  k_new == NULL: none. */
-  const void* k_new;            /* [num_new_tokens, Hkv, D] bf16 */
-  const void* v_new;            /* [num_new_tokens, Hkv, D] bf16 */
-  const int64_t* slot_mapping;  /* [num_new_tokens], slot = page * 16 + offset; < 0 skips */
-  int64_t num_new_tokens;       /* >= 0 */
+  /* Optional (NULL: none): the K and V of the call's own query rows, each [T, Hkv, D] bf16,
+   * row t belonging to query row t.  Before any key is read, row t is written into the pool
+   * at the slot that its logical position p has in its request's page table (the engine
+   * writes new tokens to their private slots before attention reads them, Section 4.1:
+   * append + attend in one call).  Rows of a skipped request, or whose page id is outside
+   * [0, num_pages), are not written.  Two requests of one call must not hold the same slot
+   * for their query rows. */
+  const void* k_new;
+  const void* v_new;
+  /* HOST hint, never value-relevant: nonzero when some pages are read by several requests
+   * of the call (a shared prefix).  K/V are then read with ordinary loads that keep them in
+   * the caches; zero streams them past the caches with non-temporal loads, the faster
+   * choice when each page is read once. */
+  int32_t shared_pages;
 } vd_attn_batch;
 
 /* Bytes of workspace one call needs for the given host-side sizes: the plan
- * (three int32 arrays of num_seqs + 1) and, for every (request, KV head,
- * query-head row < 32, 512-key split < ceil(max_context_len / 512)), a
- * partial state of head_dim + 2 floats. */
+ * (three int32 arrays of num_seqs + 1 and the split work list) and, for every
+ * (request, KV head, query-head row < 32, 512-key split < ceil(max_context_len /
+ * 512)), a partial state of head_dim + 2 floats. */
 int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
                            int32_t max_context_len, size_t* bytes);
 
 /* Paged causal attention for every row of the batch (Appendix A.2 update,
  * Section 5.3 contract).  `out` is device [T, Hq, D] bf16.  The K/V of this
- * call's own tokens must already be in the pool (vd_kv_write).  The workspace
- * holds split partial states; its prior contents do not matter.  Launches on
- * `stream` and returns without waiting. */
+ * call's own tokens must be in the pool (vd_kv_write) or be handed over in
+ * k_new / v_new.  The workspace holds the plan and the split partial states;
+ * its prior contents do not matter.  Launches on `stream` and returns without
+ * waiting. */
 int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
 
 /* The four phases vd_attn_forward runs, in this order, for callers that time
  * or schedule them separately (same batch, same output, same stream, same
  * workspace; their composition is bit-identical to vd_attn_forward):
- *   plan:   writes the batch's new tokens into the pool (when given) and,
- *           reading the per-request lengths on the device, the compact work
- *           lists of the split and chunk phases into the workspace (no
- *           device-to-host synchronisation);
+ *   plan:   only for calls with prefill rows (some s_r * (Hq / Hkv) > 32, by
+ *           the hint max_q_len) or more than 256 requests; otherwise it
+ *           launches nothing.  Writes k_new / v_new into the pool and, reading
+ *           the per-request lengths on the device, the compact work lists of
+ *           the split and chunk phases into the workspace (no device-to-host
+ *           synchronisation);
  *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
- *           per (request, KV head, 512-key split).  A request with one split
+ *           per (request, KV head, 512-key split).  Without a plan launch,
+ *           every workgroup derives its item from the lengths and the items
+ *           write the call's new tokens themselves.  A request with one split
  *           writes its output rows directly; otherwise each item writes a
  *           partial state;
  *   chunks: rows of requests with s_r * (Hq / Hkv) > 32 -- one work item per

@@ -58,11 +58,14 @@ struct Params {
   int hq, hkv, G;
   int window;  // sliding window in keys (Appendix A.5), 0 = the full causal prefix
   float c;  // softmax scale * log2(e), rounded once to fp32 on the host
-  // optional new tokens written by the plan launch
+  // optional K/V of the call's query rows ([T, Hkv, D]), written into the pool
+  // before attention reads it: by the plan launch, or (fuse_write) by the
+  // split items themselves
   const uint16_t* knew;
   const uint16_t* vnew;
-  const int64_t* slots;
-  int64_t num_new;
+  int fuse_write;
+  // the split workgroups derive their items from the lengths (no plan launch)
+  int inwave;
 };
 
 struct Req {
@@ -72,9 +75,8 @@ struct Req {
 
 // Reads request r's lengths and decides whether it may be processed without
 // touching memory outside the described buffers.
-__device__ __forceinline__ Req load_req(const Params& P, int r) {
+__device__ __forceinline__ Req make_req(const Params& P, int q0, int q1, int n) {
   Req R;
-  const int q0 = P.cu[r], q1 = P.cu[r + 1], n = P.ctx[r];
   R.q0 = q0;
   R.s = q1 - q0;
   R.n = n;
@@ -84,7 +86,19 @@ __device__ __forceinline__ Req load_req(const Params& P, int r) {
   return R;
 }
 
+__device__ __forceinline__ Req load_req(const Params& P, int r) {
+  return make_req(P, P.cu[r], P.cu[r + 1], P.ctx[r]);
+}
+
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 
 // Largest r in [0, nseq) with off[r] <= i, for a non-decreasing off[] with
 // off[0] = 0 <= i < off[nseq]: the request whose item range holds item i.
@@ -171,7 +185,22 @@ __device__ __forceinline__ void store_row(const Params& P, const f32x4 (&u)[D / 
   }
 }
 
-// Writes one (token, KV head, 8 consecutive d) of new K/V into the pools.
+// Stores 8 consecutive d (chunk dc) of one token's K and V at slot s of the
+// page block starting at element blk, in the pool layout:
+//   K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
+//   V block: element (slot, d) at ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4
+template <int D>
+__device__ __forceinline__ void put_kv8(uint16_t* kpool, uint16_t* vpool, int64_t blk, int s,
+                                        int dc, const u16x8& kv, const u16x8& vv) {
+  *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + s) * 8) = kv;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int d = 8 * dc + e;
+    vpool[blk + ((d / 16) * 4 + s / 4) * 64 + (d % 16) * 4 + s % 4] = vv[e];
+  }
+}
+
+// Writes one (token, KV head, 8 consecutive d) of new K/V to the token's slot.
 template <int D>
 __device__ __forceinline__ void kv_write_one(const uint16_t* knew, const uint16_t* vnew,
                                              const int64_t* slots, int64_t ntok, uint16_t* kpool,
@@ -186,18 +215,31 @@ __device__ __forceinline__ void kv_write_one(const uint16_t* knew, const uint16_
   const int64_t slot = slots[t];
   if (slot < 0 || slot >= num_pages * kPage) return;
   const int64_t page = slot / kPage;
-  const int s = (int)(slot % kPage);
-  const int64_t blk = (page * hkv + h) * (int64_t)(kPage * D);
   const int64_t src = (t * hkv + h) * D + 8 * dc;
-  const u16x8 kv = *reinterpret_cast<const u16x8*>(knew + src);
-  const u16x8 vv = *reinterpret_cast<const u16x8*>(vnew + src);
-  // K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
-  *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + s) * 8) = kv;
-  // V block: element (slot, d) at ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int d = 8 * dc + e;
-    vpool[blk + ((d / 16) * 4 + s / 4) * 64 + (d % 16) * 4 + s % 4] = vv[e];
+  put_kv8<D>(kpool, vpool, (page * hkv + h) * (int64_t)(kPage * D), (int)(slot % kPage), dc,
+             *reinterpret_cast<const u16x8*>(knew + src),
+             *reinterpret_cast<const u16x8*>(vnew + src));
+}
+
+// Writes query row t's K/V (every KV head) at the slot its position has in
+// its request's page table; one wavefront per row.
+template <int D>
+__device__ __forceinline__ void append_row(const Params& P, int64_t t) {
+  if (t >= P.T) return;
+  const int r = find_req(P.cu, P.num_seqs, (int)t);
+  const Req R = load_req(P, r);
+  if (!R.valid || t < R.q0 || t >= (int64_t)R.q0 + R.s) return;
+  const int p = R.n - R.s + (int)(t - R.q0);
+  const int32_t page = P.pt[(int64_t)r * P.pt_stride + p / kPage];
+  if (page < 0 || page >= P.num_pages) return;
+  uint16_t* kpool = const_cast<uint16_t*>(P.kpool);
+  uint16_t* vpool = const_cast<uint16_t*>(P.vpool);
+  for (int x = __lane_id(); x < P.hkv * (D / 8); x += 64) {
+    const int h = x / (D / 8), dc = x % (D / 8);
+    const int64_t src = (t * P.hkv + h) * D + 8 * dc;
+    put_kv8<D>(kpool, vpool, ((int64_t)page * P.hkv + h) * (kPage * D), p % kPage, dc,
+               *reinterpret_cast<const u16x8*>(P.knew + src),
+               *reinterpret_cast<const u16x8*>(P.vnew + src));
   }
 }
 
@@ -233,10 +275,8 @@ __device__ __forceinline__ void put_item(const Params& P, int64_t idx, int r, in
 template <int D>
 __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
   if (blockIdx.x > 0) {
-    // the new tokens of the call (workgroups 1..)
-    kv_write_one<D>(P.knew, P.vnew, P.slots, P.num_new, const_cast<uint16_t*>(P.kpool),
-                    const_cast<uint16_t*>(P.vpool), P.num_pages, P.hkv,
-                    (int64_t)(blockIdx.x - 1) * blockDim.x + threadIdx.x);
+    // the K/V of the call's query rows (workgroups 1..: a wavefront per row)
+    append_row<D>(P, (int64_t)(blockIdx.x - 1) * 16 + (threadIdx.x >> 6));
     return;
   }
   constexpr int NC = kPlanCounters;
@@ -370,11 +410,36 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
 // ---------------------------------------------------------------------------
 // split kernel
 // ---------------------------------------------------------------------------
+// Direct global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
+// byte address m0val + 16 l.  Issued as inline assembly so that the compiler
+// does not make every later LDS read wait for all such copies; the kernel
+// waits for them itself with wait_vmcnt.  M0 is saved and restored.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0val) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(m0val)
+      : "memory");
+}
+
 // Issue the loads of one tile's K (resp. V) operands.  Every lane loads from
 // a valid page block (a page id that is out of range or past n reads block 0
 // instead), so the load sequence is the same on every tile; the values that
 // must not be used are zeroed afterwards by mask_k / mask_v.
-template <int D>
+// NT: non-temporal loads (the data streams past the caches; each page is read
+// once), else ordinary loads (pages shared by several requests stay cached).
+template <bool NT, class V>
+__device__ __forceinline__ V load_kv(const uint16_t* p) {
+  if (NT) return __builtin_nontemporal_load(reinterpret_cast<const V*>(p));
+  return *reinterpret_cast<const V*>(p);
+}
+
+template <int D, bool NT>
 __device__ __forceinline__ void load_k(const Params& P, const int64_t (&pb)[kPagesPerTile],
                                        u16x8 (&kf)[kPagesPerTile][D / 32]) {
   const int lane = __lane_id();
@@ -383,11 +448,11 @@ __device__ __forceinline__ void load_k(const Params& P, const int64_t (&pb)[kPag
     const int64_t blk = pb[b] < 0 ? 0 : pb[b];
     const uint16_t* kb = block_ptr<D>(P.kpool, blk) + 8 * lane;
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) kf[b][ks] = *reinterpret_cast<const u16x8*>(kb + 512 * ks);
+    for (int ks = 0; ks < D / 32; ++ks) kf[b][ks] = load_kv<NT, u16x8>(kb + 512 * ks);
   }
 }
 
-template <int D>
+template <int D, bool NT>
 __device__ __forceinline__ void load_v(const Params& P, const int64_t (&pb)[kPagesPerTile],
                                        u16x4 (&vh)[D / 16][kPagesPerTile]) {
   const int lane = __lane_id();
@@ -396,7 +461,7 @@ __device__ __forceinline__ void load_v(const Params& P, const int64_t (&pb)[kPag
     const int64_t blk = pb[b] < 0 ? 0 : pb[b];
     const uint16_t* vb = block_ptr<D>(P.vpool, blk) + 4 * lane;  // = 64 grp + 4 col
 #pragma unroll
-    for (int m = 0; m < D / 16; ++m) vh[m][b] = *reinterpret_cast<const u16x4*>(vb + 256 * m);
+    for (int m = 0; m < D / 16; ++m) vh[m][b] = load_kv<NT, u16x4>(vb + 256 * m);
   }
 }
 
@@ -428,10 +493,109 @@ __device__ __forceinline__ void mask_v(const int64_t (&pb)[kPagesPerTile], int j
   }
 }
 
+// The call's new tokens on the split path (at most 16 query rows per
+// request): keys p0 = n - s .. n - 1 come from k_new / v_new (row q0 + key -
+// p0) instead of the pool, and the item that reads them also stores them to
+// their pool slots for later calls; nothing waits on these stores.
+//   K: a lane whose K row of page b is a new key loads its operand piece (16
+//      contiguous bytes) from k_new instead of the pool, in the same load
+//      instruction, and stores it to the pool address it would have read.
+//   V: before the tile's pool loads, the new rows of v_new are copied to LDS
+//      (direct global-to-LDS loads, no registers); once every load of the tile
+//      has landed, a lane's V entries of new keys are read from there.
+constexpr int kMaxNewRows = kPage;  // query rows a split item writes itself
+
+__device__ __forceinline__ bool is_new_key(int key, const Req& R) {
+  return key >= R.n - R.s && key < R.n;
+}
+
+template <int D, bool NT>
+__device__ __forceinline__ void load_k_new(const Params& P, const int64_t (&pb)[kPagesPerTile],
+                                           u16x8 (&kf)[kPagesPerTile][D / 32], int j0, int g,
+                                           const Req& R) {
+  const int lane = __lane_id(), col = lane & 15, grp = lane >> 4;
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    const int key = j0 + 16 * b + col;
+    const bool nk = is_new_key(key, R);
+    const int64_t blk = pb[b] < 0 ? 0 : pb[b];
+    const uint16_t* src =
+        nk ? P.knew + ((int64_t)(R.q0 + key - (R.n - R.s)) * P.hkv + g) * D + 8 * grp
+           : block_ptr<D>(P.kpool, blk) + 8 * lane;
+    const int stride = nk ? 32 : 512;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) kf[b][ks] = load_kv<NT, u16x8>(src + stride * ks);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_k_new(const Params& P, const int64_t (&pb)[kPagesPerTile],
+                                            const u16x8 (&kf)[kPagesPerTile][D / 32], int j0,
+                                            const Req& R) {
+  const int lane = __lane_id(), col = lane & 15;
+#pragma unroll
+  for (int b = 0; b < kPagesPerTile; ++b) {
+    if (is_new_key(j0 + 16 * b + col, R) && pb[b] >= 0) {
+      uint16_t* dst = const_cast<uint16_t*>(P.kpool) + pb[b] * (kPage * D) + 8 * lane;
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) *reinterpret_cast<u16x8*>(dst + 512 * ks) = kf[b][ks];
+    }
+  }
+}
+
+// Copies rows 0 .. s - 1 of the request's v_new (KV head g) to lds[row * D]:
+// 1 KB per copy instruction, the last row repeated into unused rows.
+template <int D>
+__device__ __forceinline__ void stage_v_new(const Params& P, uint16_t* lds, int g, const Req& R) {
+  constexpr int RPI = 64 / (D / 8);  // rows per copy
+  const int lane = __lane_id();
+  for (int c = 0; c * RPI < R.s; ++c) {
+    const int row = min(c * RPI + lane / (D / 8), R.s - 1);
+    const uint16_t* src = P.vnew + ((int64_t)(R.q0 + row) * P.hkv + g) * D + 8 * (lane % (D / 8));
+    lds_dma16(src, uni((int)(uintptr_t)(lds + c * RPI * D)));
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void apply_v_new(const Params& P, const uint16_t* lds,
+                                            const int64_t (&pb)[kPagesPerTile],
+                                            u16x4 (&vh)[D / 16][kPagesPerTile], int j0,
+                                            const Req& R) {
+  const int lane = __lane_id(), col = lane & 15, grp = lane >> 4;
+  wait_vmcnt<0>();  // the staged rows (and every load of the tile) have landed
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    // the page of the tile (at most one, s <= 16) whose slot 4 grp + i is a new key
+    int bv = -1;
+#pragma unroll
+    for (int b = 0; b < kPagesPerTile; ++b) bv = is_new_key(j0 + 16 * b + 4 * grp + i, R) ? b : bv;
+    if (bv >= 0) {
+      const uint16_t* src = lds + (j0 + 16 * bv + 4 * grp + i - (R.n - R.s)) * D + col;
+      uint16_t t[D / 16];
+#pragma unroll
+      for (int m = 0; m < D / 16; ++m) t[m] = src[16 * m];
+#pragma unroll
+      for (int b = 0; b < kPagesPerTile; ++b)
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m) vh[m][b][i] = bv == b ? t[m] : vh[m][b][i];
+      int64_t blk = -1;
+#pragma unroll
+      for (int b = 0; b < kPagesPerTile; ++b) blk = bv == b ? pb[b] : blk;
+      if (blk >= 0) {
+        uint16_t* dst = const_cast<uint16_t*>(P.vpool) + blk * (kPage * D) + 4 * lane + i;
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m) dst[256 * m] = t[m];
+      }
+    }
+  }
+}
+
 // One split item: the tiles of split k of request r, KV head g, for NA
 // column blocks of 16 query-head rows.  WIN: the handle has a sliding window.
-template <int D, int NA, bool WIN>
-__device__ __forceinline__ void split_item(const Params& P, int r, int g, int k, const Req& R) {
+// vlds: LDS rows for the call's new V rows (kMaxNewRows * D bf16).
+template <int D, int NA, bool WIN, bool NT>
+__device__ __forceinline__ void split_item(const Params& P, int r, int g, int k, const Req& R,
+                                           uint16_t* vlds) {
   const int window = WIN ? P.window : 0;
   const int lane = __lane_id();
   const int col = lane & 15, grp = lane >> 4;
@@ -452,6 +616,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
   }
 
   const int32_t* ptrow = P.pt + (int64_t)r * P.pt_stride;
+  // this call's new tokens in split k, written before any of its keys is loaded
   const int kt0 = k * kTilesPerSplit;
   const int kt_end = min(kt0 + kTilesPerSplit, (R.n + kTileKeys - 1) / kTileKeys);
   // the request's first row has the smallest window start: tiles before it
@@ -467,18 +632,27 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     const bool full = j0 + kTileKeys <= R.n && pb[0] >= 0 && pb[1] >= 0 && pb[2] >= 0 && pb[3] >= 0;
     u16x8 kf[kPagesPerTile][D / 32];
     u16x4 vh[D / 16][kPagesPerTile];
-    load_k<D>(P, pb, kf);
+    // this call's new tokens in the tile (wave-uniform)
+    const bool newtile = P.fuse_write && j0 + kTileKeys > R.n - R.s;
+    if (newtile) {
+      stage_v_new<D>(P, vlds, g, R);
+      load_k_new<D, NT>(P, pb, kf, j0, g, R);
+    } else {
+      load_k<D, NT>(P, pb, kf);
+    }
     // all K loads are issued before the V loads: Q.K can start on them first
     __builtin_amdgcn_sched_barrier(0);
-    load_v<D>(P, pb, vh);
+    load_v<D, NT>(P, pb, vh);
     const int64_t pb_cur[kPagesPerTile] = {pb[0], pb[1], pb[2], pb[3]};
     // page ids of the next tile, while this tile's loads are in flight
 #pragma unroll
     for (int b = 0; b < kPagesPerTile; ++b)
       pb[b] = page_block(P, ptrow, (kt + 1) * kPagesPerTile + b, R.n, g);
+    if (newtile) store_k_new<D>(P, pb_cur, kf, j0, R);
     if (!full) mask_k<D>(pb_cur, j0, R.n, kf);
     f32x4 acc[NA][kPagesPerTile];
     tile_scores<D, NA>([&](int b, int ks) { return kf[b][ks]; }, qf, acc);
+    if (newtile) apply_v_new<D>(P, vlds, pb_cur, vh, j0, R);
     if (!full) mask_v<D>(pb_cur, j0, R.n, vh);
     TileWeights w[NA];
     bool open = true;  // every key of the tile visible to every column
@@ -530,31 +704,180 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
   }
 }
 
-// One wavefront per workgroup: a finished item frees its slot at once, which
-// keeps the end of the launch short when item durations vary.
-template <int D, int NB, bool WIN>
-__global__ __launch_bounds__(64) void split_kernel(Params P) {
-  // the item's work-list entry: all 8 words in one scalar load, so that the
-  // exit test and the item's fields cost a single round trip (the list is
-  // read-only for the whole launch)
-  typedef int int8v __attribute__((ext_vector_type(8)));
-  const int32_t* ep = P.items + (int64_t)blockIdx.x * kItemInts;
-  int8v ev;
-  asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(ev) : "s"(ep) : "memory");
-  const int4 e0 = int4{ev[0], ev[1], ev[2], ev[3]}, e1 = int4{ev[4], ev[5], ev[6], ev[7]};
-  const int r = e0.x;
-  if (r < 0) return;
-  const int g = e0.y, k = e0.z;
+// Split items without a plan launch (calls of at most kInWaveMaxSeqs
+// requests): every workgroup reads all requests' lengths in one round trip
+// (lane l holds requests l, 64 + l, ...) and derives its own item.  Items are
+// listed per KV head -- every whole 512-key split (requests ascending, splits
+// ascending), then every last partial split, longest first (tile count 8 down
+// to 1, requests ascending) -- and each XCD (workgroup id mod 8) takes a
+// contiguous range of the list: with 8 KV heads XCD x runs head x, so a page
+// read by several requests stays in one L2, and within an XCD the shortest
+// items start last.
+constexpr int kInWaveChunks = 4;
+constexpr int kInWaveMaxSeqs = 64 * kInWaveChunks;
+
+struct SplitRef {
+  int r, g, k;
   Req R;
-  R.n = e0.w;
-  R.q0 = e1.x;
-  R.s = e1.y;
-  R.valid = true;
+};
+
+// Inclusive prefix sum over the 64 lanes with DPP moves: shifts by 1, 2, 4
+// and 8 lanes within each row of 16, then the last lane of row 0 (2) added to
+// row 1 (3), and lane 31 added to rows 2 and 3.  A lane with no source adds 0.
+__device__ __forceinline__ int wave_scan_dpp(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
+__device__ __forceinline__ bool inwave_split_item(const Params& P, SplitRef& out) {
+  constexpr int C = kInWaveChunks;
+  const int lane = __lane_id();
+  const unsigned long long below = (1ull << lane) - 1;
+  // every load first (indices clamped into [0, num_seqs)), then the arithmetic
+  int cq0[C], cq1[C], cn[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int rr = min(64 * c + lane, P.num_seqs - 1);
+    cq0[c] = P.cu[rr];
+    cq1[c] = P.cu[rr + 1];
+    cn[c] = P.ctx[rr];
+  }
+  // per request: whole-split items nf from split kfst, and the tile count cls
+  // of its last partial split (0: none)
+  int nf[C], kfst[C], cls[C], incl[C];
+  int whole = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    nf[c] = 0;
+    kfst[c] = 0;
+    cls[c] = 0;
+    incl[c] = 0;
+    if (64 * c >= P.num_seqs) continue;  // wave-uniform: no request in this chunk
+    if (64 * c + lane < P.num_seqs) {
+      const Req R = make_req(P, cq0[c], cq1[c], cn[c]);
+      if (R.valid && R.s * P.G <= P.split_cols) {
+        const int lo_min = window_lo(R.n - R.s, P.window);
+        const int nfull = R.n / kSplitKeys;
+        kfst[c] = lo_min / kSplitKeys;
+        nf[c] = max(0, nfull - kfst[c]);
+        if (R.n % kSplitKeys)
+          cls[c] = (R.n + kTileKeys - 1) / kTileKeys -
+                   max(nfull * kTilesPerSplit, lo_min / kTileKeys);
+      }
+    }
+    incl[c] = wave_scan_dpp(nf[c]);
+    whole += __builtin_amdgcn_readlane(incl[c], 63);
+  }
+  int partial = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) partial += __popcll(__ballot(cls[c] > 0));
+  const int per_head = whole + partial;
+  const int total = per_head * P.hkv;
+  const int per_xcd = (total + 7) / 8;
+  const int jx = (int)(blockIdx.x / 8);
+  if (jx >= per_xcd) return false;
+  const int i = (int)(blockIdx.x % 8) * per_xcd + jx;
+  if (i >= total) return false;
+  out.g = uni(i / per_head);
+  int idx = i - out.g * per_head;
+  const bool is_whole = idx < whole;
+  int j = -1, cj = 0, kj = 0;
+  if (is_whole) {
+    int base = 0;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const int tot = __builtin_amdgcn_readlane(incl[c], 63);
+      if (j < 0 && idx < base + tot) {
+        // the first request whose inclusive item count passes idx
+        j = __builtin_ctzll(__ballot(incl[c] > idx - base));
+        cj = c;
+        kj = __builtin_amdgcn_readlane(kfst[c], j) + idx - base -
+             __builtin_amdgcn_readlane(incl[c] - nf[c], j);
+      }
+      base += tot;
+    }
+  } else {
+    idx -= whole;
+#pragma unroll
+    for (int t = kTilesPerSplit; t >= 1; --t)
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        const unsigned long long m = __ballot(cls[c] == t);
+        const int cnt = __popcll(m);
+        if (j < 0) {
+          if (idx < cnt) {
+            // the idx-th request (ascending) of this class
+            j = __builtin_ctzll(__ballot(cls[c] == t && __popcll(m & below) == idx));
+            cj = c;
+          } else {
+            idx -= cnt;
+          }
+        }
+      }
+  }
+  if (j < 0) return false;
+  int q0 = 0, q1 = 0, n = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+    if (c == cj) {
+      q0 = __builtin_amdgcn_readlane(cq0[c], j);
+      q1 = __builtin_amdgcn_readlane(cq1[c], j);
+      n = __builtin_amdgcn_readlane(cn[c], j);
+    }
+  out.r = uni(64 * cj + j);
+  out.R = make_req(P, q0, q1, n);
+  // a whole split found above, or the request's last (partial) split
+  out.k = uni(is_whole ? kj : n / kSplitKeys);
+  // the item addresses only the request's own table row, rows and partial
+  // states: check that it is one of the request's splits
+  return out.r < P.num_seqs && out.g < P.hkv && out.R.valid && out.R.s * P.G <= P.split_cols &&
+         out.k >= window_lo(out.R.n - out.R.s, P.window) / kSplitKeys &&
+         out.k <= (out.R.n - 1) / kSplitKeys;
+}
+
+// One wavefront per workgroup: a finished item frees its slot at once, which
+// keeps the end of the launch short when item durations vary.  NT: K/V are
+// streamed with non-temporal loads.
+template <int D, int NB, bool WIN, bool NT>
+__global__ __launch_bounds__(64) void split_kernel(Params P) {
+  int r, g, k;
+  Req R;
+  if (P.inwave) {
+    SplitRef it;
+    if (!inwave_split_item(P, it)) return;
+    r = uni(it.r);
+    g = it.g;
+    k = uni(it.k);
+    R = it.R;
+  } else {
+    // the item's work-list entry: all 8 words in one scalar load, so that the
+    // exit test and the item's fields cost a single round trip (the list is
+    // read-only for the whole launch)
+    typedef int int8v __attribute__((ext_vector_type(8)));
+    const int32_t* ep = P.items + (int64_t)blockIdx.x * kItemInts;
+    int8v ev;
+    asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(ev) : "s"(ep) : "memory");
+    const int4 e0 = int4{ev[0], ev[1], ev[2], ev[3]}, e1 = int4{ev[4], ev[5], ev[6], ev[7]};
+    r = e0.x;
+    if (r < 0) return;
+    g = e0.y;
+    k = e0.z;
+    R.n = e0.w;
+    R.q0 = e1.x;
+    R.s = e1.y;
+    R.valid = true;
+  }
+  __shared__ __attribute__((aligned(16))) uint16_t vlds[kMaxNewRows * D];
   // column blocks actually used by this request: one wave-uniform dispatch
   if (NB == 2 && R.s * P.G > 16)
-    split_item<D, NB, WIN>(P, r, g, k, R);
+    split_item<D, NB, WIN, NT>(P, r, g, k, R, vlds);
   else
-    split_item<D, 1, WIN>(P, r, g, k, R);
+    split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds);
 }
 
 // Contexts of up to this many splits are merged by the short merge kernel.
@@ -729,36 +1052,12 @@ __global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
 #endif
 constexpr int kChunkStages = VD_CHUNK_STAGES;
 
-// Direct global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
-// byte address m0val + 16 l.  Issued as inline assembly so that the compiler
-// does not make every later LDS read wait for all such copies; the kernel
-// waits for them itself with wait_vmcnt.  M0 is saved and restored.
-__device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0val) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(src), "s"(m0val)
-      : "memory");
-}
-
 // Workgroup barrier that orders LDS accesses only (global memory operations
 // in flight are not waited for).
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
 // Two workgroups per CU (waves_per_eu 2: at most 256 registers per lane, and
@@ -1043,7 +1342,21 @@ int check_batch(const vd_attn* h, const vd_attn_batch* b) {
     return VD_ERR_INVALID_ARG;
   if (b->max_q_len > b->max_context_len) return VD_ERR_INVALID_ARG;
   if (b->total_q_tokens > INT32_MAX) return VD_ERR_INVALID_ARG;
+  if ((b->k_new == nullptr) != (b->v_new == nullptr)) return VD_ERR_INVALID_ARG;
   return VD_OK;
+}
+
+bool needs_chunks(const vd_attn* h, const vd_attn_batch* b) {
+  return (int64_t)b->max_q_len * h->group > kSplitCols;
+}
+
+// The plan launch runs for calls with chunk-path rows (their work list), too
+// many requests for the split workgroups to plan for themselves, or new
+// tokens of more than kMaxNewRows query rows per request (what a split item
+// writes itself).
+bool needs_plan(const vd_attn* h, const vd_attn_batch* b) {
+  return needs_chunks(h, b) || b->num_seqs > kInWaveMaxSeqs ||
+         (b->k_new != nullptr && b->max_q_len > kMaxNewRows);
 }
 
 int split_nb(const vd_attn* h, int32_t max_q_len) {
@@ -1081,11 +1394,10 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.G = h->group;
   P.window = h->window;
   P.c = h->c;
-  const bool writes = b->k_new && b->num_new_tokens > 0;
-  P.knew = writes ? static_cast<const uint16_t*>(b->k_new) : nullptr;
-  P.vnew = writes ? static_cast<const uint16_t*>(b->v_new) : nullptr;
-  P.slots = writes ? b->slot_mapping : nullptr;
-  P.num_new = writes ? b->num_new_tokens : 0;
+  P.knew = static_cast<const uint16_t*>(b->k_new);
+  P.vnew = static_cast<const uint16_t*>(b->v_new);
+  P.inwave = !needs_plan(h, b);
+  P.fuse_write = P.inwave && P.knew != nullptr;
   return P;
 }
 
@@ -1095,8 +1407,8 @@ int launched() { return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH;
 
 template <int D>
 int run_plan(const Params& P, hipStream_t s) {
-  const int64_t wthreads = P.knew ? P.num_new * P.hkv * (D / 8) : 0;
-  const int64_t blocks = 1 + (wthreads + 1023) / 1024;
+  // workgroup 0 plans; then one wavefront per query row when it has K/V to write
+  const int64_t blocks = 1 + (P.knew ? (P.T + 15) / 16 : 0);
   if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
   hipLaunchKernelGGL((plan_kernel<D>), dim3((unsigned)blocks), dim3(1024), 0, s, P);
   return launched();
@@ -1104,16 +1416,26 @@ int run_plan(const Params& P, hipStream_t s) {
 
 // Kernel launches go through hipExtLaunchKernelGGL, which records the
 // optional timing events e0 / e1 with the dispatch itself.
-template <int D>
-int run_splits(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
-  // upper bound of the split items; items past the planned total exit at once
-  const int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
-  if (items > INT32_MAX - 4) return VD_ERR_INVALID_ARG;
-  const dim3 grid((unsigned)items), block(64);
+template <int D, bool NT>
+auto split_kernel_for(const Params& P) {
   // a handle's window is fixed at creation: one kernel per handle and width
   const bool win = P.window > 0;
-  const auto kern = P.split_cols == 16 ? (win ? &split_kernel<D, 1, true> : &split_kernel<D, 1, false>)
-                                       : (win ? &split_kernel<D, 2, true> : &split_kernel<D, 2, false>);
+  return P.split_cols == 16 ? (win ? &split_kernel<D, 1, true, NT> : &split_kernel<D, 1, false, NT>)
+                            : (win ? &split_kernel<D, 2, true, NT> : &split_kernel<D, 2, false, NT>);
+}
+
+template <int D>
+int run_splits(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e0 = nullptr,
+               hipEvent_t e1 = nullptr) {
+  // upper bound of the split items; workgroups past the call's items exit at
+  // once.  Workgroups that plan for themselves take XCD-contiguous ranges of
+  // the items, so their count is a multiple of the 8 XCDs; with a work list
+  // there is exactly one workgroup per list entry.
+  int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
+  if (P.inwave) items = (items + 7) / 8 * 8;
+  if (items > INT32_MAX - 8) return VD_ERR_INVALID_ARG;
+  const dim3 grid((unsigned)items), block(64);
+  const auto kern = stream_kv ? split_kernel_for<D, true>(P) : split_kernel_for<D, false>(P);
   hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, P);
   return launched();
 }
@@ -1155,10 +1477,6 @@ int run_chunks(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent
   if (attr0 != hipSuccess || attr1 != hipSuccess) return VD_ERR_LAUNCH;
   hipExtLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), (uint32_t)lds, s, e0, e1, 0, P);
   return launched();
-}
-
-bool needs_chunks(const vd_attn* h, const vd_attn_batch* b) {
-  return (int64_t)b->max_q_len * h->group > kSplitCols;
 }
 
 bool ws_ok(const vd_attn* h, const vd_attn_batch* b, const void* ws, size_t bytes) {
@@ -1214,9 +1532,7 @@ int vd_attn_forward_plan(const vd_attn* h, const vd_attn_batch* b, void* workspa
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
-  if (b->num_new_tokens < 0 || (b->num_new_tokens > 0 && b->k_new &&
-                                 (!b->v_new || !b->slot_mapping)))
-    return VD_ERR_INVALID_ARG;
+  if (!needs_plan(h, b)) return VD_OK;  // the split workgroups plan for themselves
   const Params P = make_params(h, b, nullptr, workspace);
   return h->d == 64 ? run_plan<64>(P, stream) : run_plan<128>(P, stream);
 }
@@ -1228,7 +1544,8 @@ int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* out, 
   if (!out) return VD_ERR_INVALID_ARG;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
-  return h->d == 64 ? run_splits<64>(P, stream) : run_splits<128>(P, stream);
+  const bool nt = b->shared_pages == 0;
+  return h->d == 64 ? run_splits<64>(P, nt, stream) : run_splits<128>(P, nt, stream);
 }
 
 int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* b, void* out,
@@ -1258,8 +1575,9 @@ int vd_attn_forward_splits_timed(const vd_attn* h, const vd_attn_batch* b, void*
   if (!out) return VD_ERR_INVALID_ARG;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
-  return h->d == 64 ? run_splits<64>(P, stream, start, stop)
-                    : run_splits<128>(P, stream, start, stop);
+  const bool nt = b->shared_pages == 0;
+  return h->d == 64 ? run_splits<64>(P, nt, stream, start, stop)
+                    : run_splits<128>(P, nt, stream, start, stop);
 }
 
 int vd_attn_forward_chunks_timed(const vd_attn* h, const vd_attn_batch* b, void* out,

@@ -52,12 +52,14 @@ def fill_pool(attn: VdAttn, call: W.Call, k_pool: torch.Tensor, v_pool: torch.Te
 
 
 def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
-              hint_extra_q: int = 0, hint_extra_ctx: int = 0, append: bool = False) -> DeviceCall:
+              hint_extra_q: int = 0, hint_extra_ctx: int = 0, append: bool = False,
+              shared_pages=None) -> DeviceCall:
     """Device copy of ``call``.  Pools start as bf16 NaN (``poison``) or zero,
     then receive every valid slot; host hints are the call's true maxima plus
     the given extras.  With ``append``, this call's own tokens are not written
-    to the pool but handed to the batch (k_new, v_new, slot_mapping), for the
-    library to write before attention."""
+    to the pool but handed to the batch (k_new, v_new: the K/V of the query
+    rows), for the library to write before attention.  ``shared_pages`` is
+    set when some page is read by several requests (or as given)."""
     fill = int(np.int16(np.uint16(W.BF16_QNAN).view(np.int16))) if poison else 0
     k_pool = attn.new_pool(call.num_pages, device)
     v_pool = attn.new_pool(call.num_pages, device)
@@ -66,9 +68,8 @@ def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
     fill_pool(attn, call, k_pool, v_pool, exclude_new=append)
     extra = {}
     if append:
-        kn, vn, sl = call.new_tokens()
-        extra = dict(k_new=bf16_tensor(kn, device), v_new=bf16_tensor(vn, device),
-                     slot_mapping=torch.from_numpy(sl).to(device))
+        kn, vn = call.query_kv()
+        extra = dict(k_new=bf16_tensor(kn, device), v_new=bf16_tensor(vn, device))
     batch = Batch(
         q=bf16_tensor(call.q_bits(), device),
         cu_q_lens=torch.from_numpy(call.cu_q_lens).to(device),
@@ -76,5 +77,7 @@ def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
         page_table=torch.from_numpy(np.ascontiguousarray(call.page_table)).to(device),
         k_pool=k_pool, v_pool=v_pool, num_pages=call.num_pages,
         max_q_len=max(call.max_q_len, 1) + hint_extra_q,
-        max_context_len=max(call.max_context_len, 1) + hint_extra_ctx, **extra)
+        max_context_len=max(call.max_context_len, 1) + hint_extra_ctx,
+        shared_pages=call.shares_pages() if shared_pages is None else bool(shared_pages),
+        **extra)
     return DeviceCall(call, batch)

@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(HERE, "libvdattn.so")
 HEADER = os.path.join(ROOT, "include", "vdattn.h")
 
 VD_OK = 0
-VD_ABI_VERSION = 2
+VD_ABI_VERSION = 3
 VD_DTYPE_BF16 = 1
 TILE_KEYS = 64
 SPLIT_KEYS = 512
@@ -52,7 +52,7 @@ class _Batch(ctypes.Structure):
                 ("v_pool", ctypes.c_void_p), ("num_pages", ctypes.c_int64),
                 ("max_q_len", ctypes.c_int32), ("max_context_len", ctypes.c_int32),
                 ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p),
-                ("slot_mapping", ctypes.c_void_p), ("num_new_tokens", ctypes.c_int64)]
+                ("shared_pages", ctypes.c_int32)]
 
 
 _lib = None
@@ -146,10 +146,11 @@ class Batch:
     num_pages: int
     max_q_len: int
     max_context_len: int
-    # optional new tokens written into the pool by the plan phase
-    k_new: Optional[torch.Tensor] = None          # [N, Hkv, D] bf16
-    v_new: Optional[torch.Tensor] = None          # [N, Hkv, D] bf16
-    slot_mapping: Optional[torch.Tensor] = None   # [N] int64
+    # optional K/V of the query rows, written into the pool before attention
+    k_new: Optional[torch.Tensor] = None  # [T, Hkv, D] bf16, row t = query row t
+    v_new: Optional[torch.Tensor] = None  # [T, Hkv, D] bf16
+    # host hint: some pages are read by several requests (keeps K/V cached)
+    shared_pages: bool = False
 
 
 class VdAttn:
@@ -220,17 +221,16 @@ class VdAttn:
         _need(b.k_pool, "k_pool", torch.bfloat16, pool_elems)
         _need(b.v_pool, "v_pool", torch.bfloat16, pool_elems)
         stride = int(b.page_table.shape[1]) if B else 1
-        nnew = 0
+        if (b.k_new is None) != (b.v_new is None):
+            raise ValueError("k_new and v_new go together")
         if b.k_new is not None:
-            nnew = int(b.slot_mapping.numel())
             per = self.num_kv_heads * self.head_dim
-            _need(b.k_new, "k_new", torch.bfloat16, nnew * per)
-            _need(b.v_new, "v_new", torch.bfloat16, nnew * per)
-            _need(b.slot_mapping, "slot_mapping", torch.int64)
+            _need(b.k_new, "k_new", torch.bfloat16, T * per)
+            _need(b.v_new, "v_new", torch.bfloat16, T * per)
         return _Batch(B, T, _ptr(b.q), _ptr(b.cu_q_lens), _ptr(b.context_lens),
                       _ptr(b.page_table), stride, _ptr(b.k_pool), _ptr(b.v_pool),
                       int(b.num_pages), int(b.max_q_len), int(b.max_context_len),
-                      _ptr(b.k_new), _ptr(b.v_new), _ptr(b.slot_mapping), nnew)
+                      _ptr(b.k_new), _ptr(b.v_new), int(bool(b.shared_pages)))
 
     def _ws(self, b: Batch, workspace):
         need = self.workspace_size(int(b.context_lens.numel()), b.max_q_len, b.max_context_len)

@@ -290,6 +290,29 @@ class Call:
             return e, e.copy(), np.zeros(0, np.int64)
         return np.stack(ks), np.stack(vs), np.array(slots, np.int64)
 
+    def query_kv(self) -> Tuple[np.ndarray, np.ndarray]:
+        """K and V of the query rows, row t = query row t (position n - s + i
+        of its request): (k_rows, v_rows [T, Hkv, D] uint16)."""
+        sh = self.shape
+        if not self.reqs:
+            e = np.zeros((0, sh.num_kv_heads, sh.head_dim), np.uint16)
+            return e, e.copy()
+        k = np.concatenate([self.prompts[r.prompt].k[r.n - r.s:r.n] for r in self.reqs])
+        v = np.concatenate([self.prompts[r.prompt].v[r.n - r.s:r.n] for r in self.reqs])
+        return k, v
+
+    def shares_pages(self) -> bool:
+        """Whether some page is read by more than one request of the call."""
+        P = self.shape.page_size
+        seen = set()
+        for ri in range(len(self.reqs)):
+            n, lo = int(self.context_lens[ri]), self.first_key(ri)
+            pages = {int(self.page_table[ri, lp]) for lp in range(lo // P, -(-n // P))}
+            if pages & seen:
+                return True
+            seen |= pages
+        return False
+
     def write_list(self, exclude_new: bool = False) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
         """Every valid physical slot once: (k_rows, v_rows [W, Hkv, D] uint16,
         slot ids int64 [W] with slot = page * P + offset).  With

@@ -47,9 +47,9 @@ def test_create_supported_and_destroy(lib):
 @pytest.mark.parametrize("kw,code", [
     (dict(head_dim=96), -2), (dict(head_dim=256), -2), (dict(page_size=32), -2),
     (dict(dtype=2), -2), (dict(num_q_heads=12, num_kv_heads=8), -2),
-    (dict(num_q_heads=64, num_kv_heads=1), -2), (dict(abi_version=3), -1),
+    (dict(num_q_heads=64, num_kv_heads=1), -2), (dict(abi_version=4), -1),
     (dict(num_kv_heads=0), -1), (dict(softmax_scale=float("nan")), -1), (dict(window=-1), -1),
-    (dict(abi_version=1), -1),
+    (dict(abi_version=1), -1), (dict(abi_version=2), -1),
 ])
 def test_create_rejects(lib, kw, code):
     rc, h = _create(lib, **kw)
@@ -77,7 +77,7 @@ def test_workspace_and_pool_sizes(lib):
 def test_forward_rejects_before_launch(lib):
     rc, h = _create(lib)
     fake = 0x1000  # never dereferenced: every case below fails a host check
-    b = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, None, None, None, 0)
+    b = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, None, None, 0)
     ws = ctypes.c_size_t()
     lib.vd_attn_workspace_size(h, 1, 1, 16, ctypes.byref(ws))
     # missing workspace / too small
@@ -88,19 +88,21 @@ def test_forward_rejects_before_launch(lib):
     # null input pointers, bad sizes, inconsistent hints
     for field, val in [("q", None), ("page_table", None), ("pt_stride", 0), ("num_pages", 0),
                        ("max_q_len", 0), ("max_context_len", 0), ("num_seqs", -1)]:
-        bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, None, None, None, 0)
+        bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, None, None, 0)
         setattr(bb, field, val)
         assert lib.vd_attn_forward(h, ctypes.byref(bb), fake, fake, ws.value, None) == -1, field
-    bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 32, 16, None, None, None, 0)  # max_q > max_ctx
+    bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 32, 16, None, None, 0)  # max_q > max_ctx
     assert lib.vd_attn_forward(h, ctypes.byref(bb), fake, fake, ws.value, None) == -1
     # an empty batch is a no-op
-    e = V._Batch(0, 0, None, None, None, None, 0, None, None, 0, 0, 0, None, None, None, 0)
+    e = V._Batch(0, 0, None, None, None, None, 0, None, None, 0, 0, 0, None, None, 0)
     assert lib.vd_attn_forward(h, ctypes.byref(e), None, None, 0, None) == 0
     assert lib.vd_attn_forward(None, ctypes.byref(e), None, None, 0, None) == -1
-    # fused new tokens: negative count, or k_new without v_new / slots
-    for kn, vn, sl, cnt in [(fake, fake, fake, -1), (fake, None, fake, 3), (fake, fake, None, 3)]:
-        bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, kn, vn, sl, cnt)
-        assert lib.vd_attn_forward_plan(h, ctypes.byref(bb), fake, ws.value, None) == -1
+    # fused new tokens: k_new without v_new, or v_new without k_new
+    for kn, vn in [(fake, None), (None, fake)]:
+        bb = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, kn, vn, 0)
+        for fn in (lib.vd_attn_forward_plan,):
+            assert fn(h, ctypes.byref(bb), fake, ws.value, None) == -1
+        assert lib.vd_attn_forward(h, ctypes.byref(bb), fake, fake, ws.value, None) == -1
     # kv write
     assert lib.vd_kv_write(h, fake, fake, fake, -1, fake, fake, 4, None) == -1
     assert lib.vd_kv_write(h, None, fake, fake, 3, fake, fake, 4, None) == -1

@@ -115,6 +115,8 @@ def test_metadata_does_not_matter():
         "prepared_forward": dict(prepared="forward"),
         "prepared_phases": dict(prepared="phases"),
         "prepared_timed": dict(prepared="timed"),
+        # ordinary (cached) K/V loads instead of non-temporal ones
+        "shared_pages_hint": dict(shared_pages=True),
     }
     for name, kw in variants.items():
         U.assert_same_bits(base, U.by_position(call, U.gpu_run(call, **kw)), min_common=9)
@@ -145,6 +147,25 @@ def test_prefix_sharing_and_verify_steps():
     U.assert_same_bits(shared, copied, min_common=4 * 4 + 4)
     for step in range(4):
         U.assert_same_bits(shared, outs(W.config5(step=step, **kw)), min_common=8)
+    # non-temporal K/V loads although pages are shared
+    U.assert_same_bits(shared, outs(W.config5(shared=True, **kw), shared_pages=False),
+                       min_common=4 * 4 + 4)
+
+
+def test_large_batch_plan_launch():
+    """More than 256 requests: the plan launch lists the split items and, with
+    the query rows' K/V handed over, writes them.  A probe request gives the
+    same bits there as alone or among 17 requests, where the split workgroups
+    find their items and write the new tokens themselves."""
+    kw = dict(lo=20, hi=600)
+    solo = outs(W.config2(batch=1, probe_slot=0, **kw))
+    big = W.config2(batch=300, probe_slot=211, perm_stream=5, **kw)
+    U.assert_same_bits(solo, outs(big))
+    out_append = U.gpu_run(big, append=True)
+    U.assert_same_bits(solo, U.by_position(big, out_append))
+    U.assert_same_bits(outs(big), U.by_position(big, out_append), min_common=300)
+    U.assert_same_bits(solo, outs(W.config2(batch=17, probe_slot=3, **kw), append=True))
+    U.say("  300 requests, appended: %s" % U.parity(big, out_append, rows=[0, 150, 211, 299]))
 
 
 def test_long_context_batch_and_placement():

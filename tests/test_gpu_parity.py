@@ -169,9 +169,10 @@ def test_parity_full_size_verify_sampled():
 
 @pytest.mark.parametrize("name", ["cfg1_tiny", "cfg3_mixed_small", "cfg5_verify_small"])
 def test_append_then_attend(name):
-    """The call's own tokens handed to vd_attn_forward (written by its plan
-    phase) instead of written beforehand with vd_kv_write: the same bits, and
-    within tolerance of the oracle."""
+    """The call's own tokens handed to vd_attn_forward (written by the split
+    items themselves, or by the plan launch when the call has prefill rows)
+    instead of written beforehand with vd_kv_write: the same bits, and within
+    tolerance of the oracle."""
     call = SMALL[name]()
     a = U.gpu_run(call, append=True)
     b = U.gpu_run(call)
