@@ -221,25 +221,83 @@ __device__ __forceinline__ void kv_write_one(const uint16_t* knew, const uint16_
              *reinterpret_cast<const u16x8*>(vnew + src));
 }
 
-// Writes query row t's K/V (every KV head) at the slot its position has in
-// its request's page table; one wavefront per row.
+// Writes the K/V of the call's query rows (every KV head) at the slots their
+// positions have in the request's page table.  The wavefront of query row t
+// writes the rows of t's 4-slot group (positions p .. up to the next multiple
+// of 4), when t is the request's first row or starts such a group; the V
+// layout keeps 4 consecutive slots of one d contiguous, so a whole group is
+// written with 8-byte stores.
 template <int D>
-__device__ __forceinline__ void append_row(const Params& P, int64_t t) {
+__device__ __forceinline__ void append_rows(const Params& P, int64_t t) {
   if (t >= P.T) return;
   const int r = find_req(P.cu, P.num_seqs, (int)t);
   const Req R = load_req(P, r);
   if (!R.valid || t < R.q0 || t >= (int64_t)R.q0 + R.s) return;
-  const int p = R.n - R.s + (int)(t - R.q0);
+  const int p0 = R.n - R.s;
+  const int p = p0 + (int)(t - R.q0);
+  if (p != p0 && (p & 3) != 0) return;  // written by the wavefront of its group's first row
+  const int cnt = min(R.n, (p & ~3) + 4) - p;  // rows t .. t + cnt - 1
   const int32_t page = P.pt[(int64_t)r * P.pt_stride + p / kPage];
   if (page < 0 || page >= P.num_pages) return;
+  const int slot0 = p % kPage;
+  const int lane = __lane_id();
+  const int64_t rs = (int64_t)P.hkv * D;  // elements per row of k_new / v_new
   uint16_t* kpool = const_cast<uint16_t*>(P.kpool);
   uint16_t* vpool = const_cast<uint16_t*>(P.vpool);
-  for (int x = __lane_id(); x < P.hkv * (D / 8); x += 64) {
-    const int h = x / (D / 8), dc = x % (D / 8);
-    const int64_t src = (t * P.hkv + h) * D + 8 * dc;
-    put_kv8<D>(kpool, vpool, ((int64_t)page * P.hkv + h) * (kPage * D), p % kPage, dc,
-               *reinterpret_cast<const u16x8*>(P.knew + src),
-               *reinterpret_cast<const u16x8*>(P.vnew + src));
+  // Loads are issued in batches of B before their stores (the compiler must
+  // assume that the pool stores may alias k_new / v_new).
+  constexpr int B = 8;
+  // K: one 16-byte piece per (row, head, 8 d): element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
+  const int nk = cnt * P.hkv * (D / 8);
+  for (int x0 = 0; x0 < nk; x0 += 64 * B) {
+    u16x8 v[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int x = x0 + 64 * u + lane;
+      if (x < nk) {
+        const int i = x / (P.hkv * (D / 8)), hd = x % (P.hkv * (D / 8));
+        v[u] = *reinterpret_cast<const u16x8*>(P.knew + (t + i) * rs + hd * 8);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int x = x0 + 64 * u + lane;
+      if (x < nk) {
+        const int i = x / (P.hkv * (D / 8)), hd = x % (P.hkv * (D / 8));
+        const int h = hd / (D / 8), dc = hd % (D / 8);
+        const int64_t blk = ((int64_t)page * P.hkv + h) * (kPage * D);
+        *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + slot0 + i) * 8) = v[u];
+      }
+    }
+  }
+  // V: per (head, d) the group's values: element (slot, d) at
+  // ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4
+  const int nv = P.hkv * D;
+  for (int x0 = 0; x0 < nv; x0 += 64 * B) {
+    u16x4 v[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int x = x0 + 64 * u + lane;
+      if (x < nv) {
+        const uint16_t* src = P.vnew + t * rs + x;  // x = h * D + d
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[u][i] = i < cnt ? src[i * rs] : (uint16_t)0;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int x = x0 + 64 * u + lane;
+      if (x < nv) {
+        const int h = x / D, d = x % D;
+        uint16_t* dst = vpool + ((int64_t)page * P.hkv + h) * (kPage * D) +
+                        ((d / 16) * 4 + slot0 / 4) * 64 + (d % 16) * 4 + slot0 % 4;
+        if (cnt == 4) {  // a whole group (slot0 % 4 == 0)
+          *reinterpret_cast<u16x4*>(dst) = v[u];
+        } else {
+          for (int i = 0; i < cnt; ++i) dst[i] = v[u][i];
+        }
+      }
+    }
   }
 }
 
@@ -276,9 +334,10 @@ template <int D>
 __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
   if (blockIdx.x > 0) {
     // the K/V of the call's query rows (workgroups 1..: a wavefront per row)
-    append_row<D>(P, (int64_t)(blockIdx.x - 1) * 16 + (threadIdx.x >> 6));
+    append_rows<D>(P, (int64_t)(blockIdx.x - 1) * 16 + (threadIdx.x >> 6));
     return;
   }
+  if (P.inwave) return;  // the split and chunk workgroups plan for themselves
   constexpr int NC = kPlanCounters;
   __shared__ int wsum[NC][16];  // per-wavefront totals of each counter
   __shared__ int wpre[NC][16];  // offset of each (counter, wavefront)
@@ -840,6 +899,73 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, SplitRef& out
          out.k <= (out.R.n - 1) / kSplitKeys;
 }
 
+// Chunk items without a plan launch (at most kInWaveMaxSeqs requests): the
+// same one-round-trip read of the lengths, and the items of the plan's chunk
+// list -- per KV head, every q-tile of 128 query-head rows of every request
+// on the chunk path, requests ascending -- with XCD-contiguous ranges.
+__device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& r, int& qt,
+                                                  Req& R) {
+  constexpr int C = kInWaveChunks;
+  const int lane = __lane_id();
+  int cq0[C], cq1[C], cn[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int rr = min(64 * c + lane, P.num_seqs - 1);
+    cq0[c] = P.cu[rr];
+    cq1[c] = P.cu[rr + 1];
+    cn[c] = P.ctx[rr];
+  }
+  int cnt[C], incl[C];
+  int per_head = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    cnt[c] = 0;
+    incl[c] = 0;
+    if (64 * c >= P.num_seqs) continue;
+    if (64 * c + lane < P.num_seqs) {
+      const Req Rl = make_req(P, cq0[c], cq1[c], cn[c]);
+      const int ncols = Rl.s * P.G;
+      if (Rl.valid && ncols > P.split_cols) cnt[c] = (ncols + kChunkCols - 1) / kChunkCols;
+    }
+    incl[c] = wave_scan_dpp(cnt[c]);
+    per_head += __builtin_amdgcn_readlane(incl[c], 63);
+  }
+  const int total = per_head * P.hkv;
+  const int per_xcd = (total + 7) / 8;
+  const int jx = (int)(blockIdx.x / 8);
+  if (jx >= per_xcd) return false;
+  const int i = (int)(blockIdx.x % 8) * per_xcd + jx;
+  if (i >= total) return false;
+  g = uni(i / per_head);
+  const int rem = i - g * per_head;
+  int j = -1, cj = 0, off = 0, base = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int tot = __builtin_amdgcn_readlane(incl[c], 63);
+    if (j < 0 && rem < base + tot) {
+      j = __builtin_ctzll(__ballot(incl[c] > rem - base));
+      cj = c;
+      off = rem - base - __builtin_amdgcn_readlane(incl[c] - cnt[c], j);
+    }
+    base += tot;
+  }
+  if (j < 0) return false;
+  int q0 = 0, q1 = 0, n = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+    if (c == cj) {
+      q0 = __builtin_amdgcn_readlane(cq0[c], j);
+      q1 = __builtin_amdgcn_readlane(cq1[c], j);
+      n = __builtin_amdgcn_readlane(cn[c], j);
+    }
+  r = uni(64 * cj + j);
+  qt = uni(off);
+  R = make_req(P, q0, q1, n);
+  const int ncols = R.s * P.G;
+  return r < P.num_seqs && g < P.hkv && R.valid && ncols > P.split_cols &&
+         qt < (ncols + kChunkCols - 1) / kChunkCols;
+}
+
 // One wavefront per workgroup: a finished item frees its slot at once, which
 // keeps the end of the launch short when item durations vary.  NT: K/V are
 // streamed with non-temporal loads.
@@ -884,11 +1010,12 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
 constexpr int kShortMerge = 16;
 
 // ---------------------------------------------------------------------------
-// short merge (contexts of at most 16 splits): one thread per (request, KV
-// head, column, 4 consecutive d), folding the partial states in ascending
-// split order with fold_scalars / fold_value.
+// short merge (contexts of at most KS <= 16 splits): one thread per (request,
+// KV head, column, 4 consecutive d), folding the partial states in ascending
+// split order with fold_scalars / fold_value; KS (4, 8 or 16) sizes the
+// registers for the call's split count.
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, int KS>
 __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int per_rg = cols * (D / 4);
@@ -902,18 +1029,16 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   const int ncols = R.s * P.G;
   if (ncols > P.split_cols || c >= ncols) return;
   if (request_splits(R, P.window) == 1) return;  // written by the split kernel
-  const int MS = P.max_splits;
   // the row's splits: from the one holding its window start through its own
   const int pr = R.n - R.s + c / P.G;
   const int klo = window_lo(pr, P.window) / kSplitKeys;
   const int kp = pr / kSplitKeys + 1 - klo;
-  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS + klo;
-  // every partial state is loaded first (at most kShortMerge of them), then
-  // folded in ascending split order
-  float mk[kShortMerge], zk[kShortMerge];
-  f32x4 uk[kShortMerge];
+  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * P.max_splits + klo;
+  // every partial state is loaded first, then folded in ascending split order
+  float mk[KS], zk[KS];
+  f32x4 uk[KS];
 #pragma unroll
-  for (int k = 0; k < kShortMerge; ++k) {
+  for (int k = 0; k < KS; ++k) {
     if (k < kp) {
       mk[k] = P.ws_m[p0 + k];
       zk[k] = P.ws_z[p0 + k];
@@ -923,7 +1048,7 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   float M = mk[0], Z = zk[0];
   f32x4 W = uk[0];
 #pragma unroll
-  for (int k = 1; k < kShortMerge; ++k) {
+  for (int k = 1; k < KS; ++k) {
     if (k < kp) {
       const FoldScalars f = fold_scalars(M, Z, mk[k], zk[k]);
 #pragma unroll
@@ -939,103 +1064,75 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   *reinterpret_cast<u16x4*>(P.out + ((int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G) * D + d) = o;
 }
 
+__device__ __forceinline__ float readlane_f(float v, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+
 // ---------------------------------------------------------------------------
-// merge kernel: one workgroup of 256 threads per
-// (request, KV head, slice of 256 output elements).  The fold is the same left
-// fold as fold_scalars / fold_value, evaluated in 64-split chunks: the running
-// maximum is an exact prefix maximum, so the two exp2 factors of every step
-// are computed in parallel; the Z and W recurrences stay sequential in k.
+// long merge (more than 16 splits): one wavefront per (request, KV head,
+// column, 64 consecutive d).  The splits are taken in chunks of 64: lane k
+// loads split k's (m, z), the running maximum through every split is an exact
+// prefix maximum, so both exp2 factors of every fold step are computed in
+// parallel; each lane loads its d of all 64 partial U vectors at once, and the
+// left fold of fold_scalars / fold_value then runs in ascending split order
+// with the factors read from their lanes.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void merge_kernel(Params P, int slices) {
+__global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
   constexpr int CH = 64;
-  constexpr int SC = 256 / D + 1;  // columns a slice can touch
-  __shared__ float sa[SC][CH], sb[SC][CH], sz[SC][CH];
-  __shared__ float sM[SC], sZ[SC];
-  const int64_t bid = blockIdx.x;
-  const int slice = (int)(bid % slices);
-  const int64_t rg = bid / slices;
+  const int64_t id = blockIdx.x;
+  const int per_rg = cols * (D / 64);
+  const int64_t rg = id / per_rg;
   if (rg >= (int64_t)P.num_seqs * P.hkv) return;
+  const int rem = (int)(id % per_rg);
+  const int c = rem / (D / 64), d = 64 * (rem % (D / 64)) + __lane_id();
   const int r = (int)(rg / P.hkv), g = (int)(rg % P.hkv);
+  const int lane = __lane_id();
   const Req R = load_req(P, r);
   if (!R.valid) return;
   const int ncols = R.s * P.G;
-  if (ncols > P.split_cols) return;
-  const int nsplit = request_splits(R, P.window);  // bounds every row's split count
-  if (nsplit == 1) return;  // written by the split kernel
-  const int e0 = slice * 256;
-  if (e0 >= ncols * D) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int cfirst = e0 / D;
-  const int clast = (min(ncols * D, e0 + 256) - 1) / D;
-  const int ncs = clast - cfirst + 1;
-  const int MS = P.max_splits;
-  const int64_t base = (int64_t)(r * P.hkv + g) * kSplitCols * MS;
-  const int e = e0 + tid;
-  const bool mine = e < ncols * D;
-  const int c = mine ? e / D : cfirst;
-  const int d = e % D;
-  // row c's splits: from the one holding its window start through its own
+  if (ncols > P.split_cols || c >= ncols) return;
+  if (request_splits(R, P.window) == 1) return;  // written by the split kernel
+  // the row's splits: from the one holding its window start through its own
   const int pr = R.n - R.s + c / P.G;
   const int klo = window_lo(pr, P.window) / kSplitKeys;
   const int kp = pr / kSplitKeys + 1 - klo;
-  const int64_t pu = (base + (int64_t)c * MS + klo) * D + d;
-  float W = 0.f;
-  for (int k0 = 0; k0 < nsplit; k0 += CH) {
-    // per-column factors of this chunk: wavefront w takes columns w, w + 4, ...
-    for (int ci = wave; ci < ncs; ci += 4) {
-      const int cc = cfirst + ci;
-      const int pc = R.n - R.s + cc / P.G;
-      const int kloc = window_lo(pc, P.window) / kSplitKeys;
-      const int kpc = pc / kSplitKeys + 1 - kloc;
-      const int64_t p0 = base + (int64_t)cc * MS + kloc;
-      const int k = k0 + lane;
-      const bool has = k < kpc;
-      const float mk = has ? P.ws_m[p0 + k] : -__builtin_inff();
-      const float zk = has ? P.ws_z[p0 + k] : 0.0f;
-      const float carry = k0 == 0 ? -__builtin_inff() : sM[ci];
-      float pm = mk;  // inclusive prefix maximum over the chunk
+  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * P.max_splits + klo;
+  float carry = -__builtin_inff();  // running maximum before the chunk
+  float Z = 0.f, W = 0.f;
+  for (int k0 = 0; k0 < kp; k0 += CH) {
+    const bool has = k0 + lane < kp;
+    const float mk = has ? P.ws_m[p0 + k0 + lane] : -__builtin_inff();
+    const float zk = has ? P.ws_z[p0 + k0 + lane] : 0.0f;
+    float u[CH];
 #pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const float t = __shfl_up(pm, o, 64);
-        if (lane >= o) pm = fmax_(pm, t);
-      }
-      const float Mk = fmax_(carry, pm);
-      float Mp = __shfl_up(Mk, 1, 64);
-      if (lane == 0) Mp = carry;
-      sa[ci][lane] = ex2(Mp - Mk);
-      sb[ci][lane] = ex2(mk - Mk);
-      sz[ci][lane] = zk;
-      const float Mlast = __shfl(Mk, 63, 64);
-      if (lane == 0) {
-        // Z recurrence of this chunk (sequential, as fold_scalars)
-        float Z = k0 == 0 ? zk : sZ[ci];
-        const int kend = min(CH, kpc - k0);
-        for (int kk = k0 == 0 ? 1 : 0; kk < kend; ++kk) Z = Z * sa[ci][kk] + sz[ci][kk] * sb[ci][kk];
-        sZ[ci] = Z;
-        sM[ci] = Mlast;
+    for (int j = 0; j < CH; ++j) u[j] = k0 + j < kp ? P.ws_u[(p0 + k0 + j) * D + d] : 0.0f;
+    float pm = mk;  // inclusive prefix maximum over the chunk
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const float t = __shfl_up(pm, o, 64);
+      if (lane >= o) pm = fmax_(pm, t);
+    }
+    const float Mk = fmax_(carry, pm);  // M after split k0 + lane
+    float Mp = __shfl_up(Mk, 1, 64);    // M before it
+    if (lane == 0) Mp = carry;
+    const float a = ex2(Mp - Mk), b = ex2(mk - Mk);
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      if (k0 + j < kp) {
+        if (k0 + j == 0) {
+          W = u[0];
+          Z = readlane_f(zk, 0);
+        } else {
+          const float aj = readlane_f(a, j), bj = readlane_f(b, j);
+          Z = Z * aj + readlane_f(zk, j) * bj;
+          W = fold_value(W, u[j], FoldScalars{0.f, 0.f, aj, bj});
+        }
       }
     }
-    __syncthreads();
-    if (mine) {
-      const int kend = min(CH, kp - k0);
-      const int ci = c - cfirst;
-      float u[CH];
-#pragma unroll
-      for (int kk = 0; kk < CH; ++kk) u[kk] = kk < kend ? P.ws_u[pu + (int64_t)(k0 + kk) * D] : 0.0f;
-      if (k0 == 0) W = u[0];
-      const int kbeg = k0 == 0 ? 1 : 0;
-#pragma unroll
-      for (int kk = 0; kk < CH; ++kk)
-        if (kk >= kbeg && kk < kend)
-          W = fold_value(W, u[kk], FoldScalars{0.f, 0.f, sa[ci][kk], sb[ci][kk]});
-    }
-    __syncthreads();
+    carry = readlane_f(Mk, CH - 1);
   }
-  if (mine) {
-    const float rho = final_scale(sZ[c - cfirst]);
-    P.out[((int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G) * D + d] = bf16_out(W * rho);
-  }
+  P.out[((int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G) * D + d] = bf16_out(W * final_scale(Z));
 }
 
 // ---------------------------------------------------------------------------
@@ -1082,19 +1179,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // id mod 8) take a contiguous range of them: the q-tiles of one (request,
   // KV head) share that XCD's L2, and with 8 KV heads each XCD takes one head
   // of every request, so long and short requests spread over all XCDs.
-  const int per_head = P.off_chunk[P.num_seqs];
-  const int total = per_head * P.hkv;
-  const int per_xcd = (total + 7) / 8;
-  const int jx = (int)(blockIdx.x / 8);
-  if (jx >= per_xcd) return;
-  const int i = uni((int)(blockIdx.x % 8) * per_xcd + jx);
-  if (i >= total) return;
-  const int g = uni(i / per_head);
-  const int rem = i - g * per_head;
-  const int r = find_req(P.off_chunk, P.num_seqs, rem);
-  const Req R = load_req(P, r);
+  int g, r, qt;
+  Req R;
+  if (P.inwave) {
+    if (!inwave_chunk_item(P, g, r, qt, R)) return;
+  } else {
+    const int per_head = P.off_chunk[P.num_seqs];
+    const int total = per_head * P.hkv;
+    const int per_xcd = (total + 7) / 8;
+    const int jx = (int)(blockIdx.x / 8);
+    if (jx >= per_xcd) return;
+    const int i = uni((int)(blockIdx.x % 8) * per_xcd + jx);
+    if (i >= total) return;
+    g = uni(i / per_head);
+    const int rem = i - g * per_head;
+    r = find_req(P.off_chunk, P.num_seqs, rem);
+    R = load_req(P, r);
+    qt = uni(rem - P.off_chunk[r]);
+  }
   const int ncols = R.s * P.G;
-  const int qt = uni(rem - P.off_chunk[r]);
   const int c0 = qt * kChunkCols;
   const int cend = min(ncols, c0 + kChunkCols);
   const int pmax = R.n - R.s + (cend - 1) / P.G;  // last position of the block
@@ -1350,13 +1453,21 @@ bool needs_chunks(const vd_attn* h, const vd_attn_batch* b) {
   return (int64_t)b->max_q_len * h->group > kSplitCols;
 }
 
-// The plan launch runs for calls with chunk-path rows (their work list), too
-// many requests for the split workgroups to plan for themselves, or new
-// tokens of more than kMaxNewRows query rows per request (what a split item
-// writes itself).
+// Calls of at most kInWaveMaxSeqs requests need no work lists: the split and
+// chunk workgroups derive their items from the lengths.
+bool plans_inwave(const vd_attn_batch* b) { return b->num_seqs <= kInWaveMaxSeqs; }
+
+// The split items write the call's new tokens themselves when every row is on
+// the split path, with at most kMaxNewRows query rows per request.
+bool fuses_write(const vd_attn* h, const vd_attn_batch* b) {
+  return b->k_new != nullptr && plans_inwave(b) && !needs_chunks(h, b) &&
+         b->max_q_len <= kMaxNewRows;
+}
+
+// The plan launch runs for the work lists of a call with more requests, and
+// for new tokens the split items do not write.
 bool needs_plan(const vd_attn* h, const vd_attn_batch* b) {
-  return needs_chunks(h, b) || b->num_seqs > kInWaveMaxSeqs ||
-         (b->k_new != nullptr && b->max_q_len > kMaxNewRows);
+  return !plans_inwave(b) || (b->k_new != nullptr && !fuses_write(h, b));
 }
 
 int split_nb(const vd_attn* h, int32_t max_q_len) {
@@ -1396,8 +1507,8 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.c = h->c;
   P.knew = static_cast<const uint16_t*>(b->k_new);
   P.vnew = static_cast<const uint16_t*>(b->v_new);
-  P.inwave = !needs_plan(h, b);
-  P.fuse_write = P.inwave && P.knew != nullptr;
+  P.inwave = plans_inwave(b);
+  P.fuse_write = fuses_write(h, b);
   return P;
 }
 
@@ -1407,8 +1518,9 @@ int launched() { return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH;
 
 template <int D>
 int run_plan(const Params& P, hipStream_t s) {
-  // workgroup 0 plans; then one wavefront per query row when it has K/V to write
-  const int64_t blocks = 1 + (P.knew ? (P.T + 15) / 16 : 0);
+  // workgroup 0 plans (unless the workgroups plan for themselves); then one
+  // wavefront per query row when the call's new tokens are written here
+  const int64_t blocks = 1 + (P.knew && !P.fuse_write ? (P.T + 15) / 16 : 0);
   if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
   hipLaunchKernelGGL((plan_kernel<D>), dim3((unsigned)blocks), dim3(1024), 0, s, P);
   return launched();
@@ -1447,14 +1559,16 @@ int run_merge(const Params& P, hipStream_t s) {
     const int64_t threads = (int64_t)P.num_seqs * P.hkv * cols * (D / 4);
     const int64_t blocks = (threads + 255) / 256;
     if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
-    hipLaunchKernelGGL((merge_short_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, s, P,
-                       (int)cols);
+    // registers for the call's split count: 4, 8 or 16 partial states
+    const auto kern = P.max_splits <= 4   ? &merge_short_kernel<D, 4>
+                      : P.max_splits <= 8 ? &merge_short_kernel<D, 8>
+                                          : &merge_short_kernel<D, 16>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, s, P, (int)cols);
     return launched();
   }
-  const int slices = (int)((cols * D + 255) / 256);
-  const int64_t blocks = (int64_t)P.num_seqs * P.hkv * slices;
+  const int64_t blocks = (int64_t)P.num_seqs * P.hkv * cols * (D / 64);
   if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
-  hipLaunchKernelGGL((merge_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, s, P, slices);
+  hipLaunchKernelGGL((merge_long_kernel<D>), dim3((unsigned)blocks), dim3(64), 0, s, P, (int)cols);
   return launched();
 }
 

@@ -166,6 +166,15 @@ def test_large_batch_plan_launch():
     U.assert_same_bits(outs(big), U.by_position(big, out_append), min_common=300)
     U.assert_same_bits(solo, outs(W.config2(batch=17, probe_slot=3, **kw), append=True))
     U.say("  300 requests, appended: %s" % U.parity(big, out_append, rows=[0, 150, 211, 299]))
+    # prefill rows too: the plan launch's chunk list (263 requests) against the
+    # chunk workgroups' own planning (13 requests)
+    kw3 = dict(num_prefill=3, chunk=96, max_off=900, dec_lo=20, dec_hi=400)
+    small = outs(W.config3(num_decode=10, **kw3))
+    large = W.config3(num_decode=260, **kw3)
+    U.assert_same_bits(small, outs(large), min_common=3 * 96 + 10)
+    U.assert_same_bits(small, outs(large, append=True), min_common=3 * 96 + 10)
+    U.assert_same_bits(small, outs(W.config3(num_decode=10, **kw3), append=True),
+                       min_common=3 * 96 + 10)
 
 
 def test_long_context_batch_and_placement():
