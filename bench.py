@@ -1,11 +1,13 @@
 """Benchmark of the paged-attention hot path on one MI355X.
 
 A step is one pass of the whole path over one batch: the KV-cache write of
-the batch's new tokens followed by attention, i.e. the plan phase (which also
-writes the new tokens into the pool), then the split, chunk and merge phases
-of vd_attn_forward, on synthetic bf16 inputs already resident in HBM.  R replicas of the inputs (pools, page tables, queries) are
-cycled so that no step finds its K/V in the 256 MB last-level cache left
-behind by the previous step.
+the batch's new tokens followed by attention, i.e. the phases of
+vd_attn_forward -- plan (launched only when the batch needs it: prefill rows,
+whose new tokens it writes, or more than 256 requests), split, chunk and merge
+-- on synthetic bf16 inputs already resident in HBM; on a decode batch the
+split items write the new tokens themselves.  R replicas of the inputs (pools,
+page tables, queries) are cycled so that no step finds its K/V in the 256 MB
+last-level cache left behind by the previous step.
 
 Prints one JSON line: whole-step KV GB/s (algorithmic K+V bytes of the batch
 over the step time), the roofline of the dominant kernel measured with HIP
@@ -262,8 +264,14 @@ def main():
                 "avg_ms": round(dom_ms, 5), "timed_launches": len(evs),
                 "algorithmic_flop": int(chunk_flops)}
     else:
+        # K+V of the visible keys, Q, the page-table entries read; and when the
+        # split items write the call's new tokens themselves (every row on the
+        # split path, at most 16 query rows per request, at most 256 requests),
+        # the new K+V rows read from k_new / v_new and written to the pool
         alg = split_bytes + sum(r.s for r in split_reqs) * hq * D * 2 + \
             sum(-(-r.n // P) - call.first_key(i) // P for i, r in zip(split_idx, split_reqs)) * 4
+        if len(split_reqs) == call.num_seqs <= 256 and call.max_q_len <= 16:
+            alg += 2 * T * hkv * D * 2 * 2
         ach = alg / (dom_ms * 1e-3) / 1e9
         roof = {"kernel": "split_kernel", "bound": "hbm", "achieved": round(ach, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
