@@ -134,7 +134,8 @@ __device__ __forceinline__ int window_lo(int p, int w) {
 struct TileWeights {
   u16x8 pf[2];
   float alpha, m_new, z_new;
-  bool h;
+  uint32_t h;  // 0 or 1; a 32-bit field like the others (a bool here is kept
+               // as bytes by the compiler and repacked on every tile)
 };
 
 //
