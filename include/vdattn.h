@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define VD_ABI_VERSION 3
+#define VD_ABI_VERSION 4
 
 typedef enum {
   VD_OK = 0,
@@ -126,6 +126,12 @@ typedef struct {
    * the caches; zero streams them past the caches with non-temporal loads, the faster
    * choice when each page is read once. */
   int32_t shared_pages;
+  /* Optional output (NULL: not written): [T, Hq] fp32, row t's log-sum-exp in natural log,
+   * ln sum_j exp(scale * q.k_j) over the keys the row sees.  The tile update of Appendix A.2
+   * carries it as the state (m, z); the paper does not export it.  It is what a caller needs
+   * to merge this attention with attention over other keys, and it is bit-invariant like
+   * the output (it depends only on the row's final (m, z)). */
+  float* lse;
 } vd_attn_batch;
 
 /* Bytes of workspace one call needs for the given host-side sizes: the plan

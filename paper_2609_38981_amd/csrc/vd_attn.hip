@@ -66,6 +66,7 @@ struct Params {
   int fuse_write;
   // the split workgroups derive their items from the lengths (no plan launch)
   int inwave;
+  float* lse;  // optional [T, Hq] log-sum-exp output
 };
 
 struct Req {
@@ -170,11 +171,13 @@ __device__ __forceinline__ int request_splits(const Req& R, int window) {
 }
 
 // Stores one column's output row from its accumulator blocks (lane layout of
-// the U accumulator: d = 16 m + 4 grp + i).
+// the U accumulator: d = 16 m + 4 grp + i), and its log-sum-exp when asked.
 template <int D>
-__device__ __forceinline__ void store_row(const Params& P, const f32x4 (&u)[D / 16], float rho,
-                                          int64_t tok, int head) {
+__device__ __forceinline__ void store_row(const Params& P, const f32x4 (&u)[D / 16], float M,
+                                          float Z, int64_t tok, int head) {
   const int grp = __lane_id() >> 4;
+  const float rho = final_scale(Z);
+  if (P.lse && grp == 0) P.lse[tok * P.hq + head] = final_lse(M, Z);
   uint16_t* o = P.out + (tok * P.hq + head) * D + 4 * grp;
 #pragma unroll
   for (int m = 0; m < D / 16; ++m) {
@@ -743,7 +746,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     for (int nb = 0; nb < NA; ++nb) {
       if (pos[nb] < 0) continue;
       const int c = nb * 16 + col;
-      store_row<D>(P, st[nb].u, final_scale(st[nb].z), R.q0 + c / P.G, g * P.G + c % P.G);
+      store_row<D>(P, st[nb].u, st[nb].m, st[nb].z, R.q0 + c / P.G, g * P.G + c % P.G);
     }
     return;
   }
@@ -1061,7 +1064,9 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   u16x4 o;
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = bf16_out(W[i] * rho);
-  *reinterpret_cast<u16x4*>(P.out + ((int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G) * D + d) = o;
+  const int64_t row = (int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G;
+  *reinterpret_cast<u16x4*>(P.out + row * D + d) = o;
+  if (P.lse && d == 0) P.lse[row] = final_lse(M, Z);
 }
 
 __device__ __forceinline__ float readlane_f(float v, int lane) {
@@ -1132,7 +1137,9 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
     }
     carry = readlane_f(Mk, CH - 1);
   }
-  P.out[((int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G) * D + d] = bf16_out(W * final_scale(Z));
+  const int64_t row = (int64_t)(R.q0 + c / P.G) * P.hq + g * P.G + c % P.G;
+  P.out[row * D + d] = bf16_out(W * final_scale(Z));
+  if (P.lse && d == 0) P.lse[row] = final_lse(carry, Z);  // carry: the maximum over every split
 }
 
 // ---------------------------------------------------------------------------
@@ -1374,7 +1381,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   for (int nb = 0; nb < NB; ++nb) {
     if (pos[nb] < 0) continue;
     const int c = c0 + wave * 32 + nb * 16 + col;
-    store_row<D>(P, W[nb], final_scale(Z[nb]), R.q0 + c / P.G, g * P.G + c % P.G);
+    store_row<D>(P, W[nb], M[nb], Z[nb], R.q0 + c / P.G, g * P.G + c % P.G);
   }
 }
 
@@ -1508,6 +1515,7 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.knew = static_cast<const uint16_t*>(b->k_new);
   P.vnew = static_cast<const uint16_t*>(b->v_new);
   P.inwave = plans_inwave(b);
+  P.lse = b->lse;
   P.fuse_write = fuses_write(h, b);
   return P;
 }

@@ -241,4 +241,13 @@ __device__ __forceinline__ float fold_value(float W, float uk, const FoldScalars
 // Final normalisation: o = cast(W * select(Z > 0, 1 / Z, 0)), IEEE division.
 __device__ __forceinline__ float final_scale(float Z) { return Z > 0.0f ? 1.0f / Z : 0.0f; }
 
+// Log-sum-exp of the row's visible scaled scores, in natural log: the state
+// (M, Z) holds M = the largest base-two score c * dot and Z = the sum of
+// exp2(score - M) (at least 1 for a row with a visible key), so
+// ln sum exp(scale * dot) = (M + log2 Z) * ln 2; log2 is v_log_f32.
+constexpr float kLn2 = 0.693147180559945309417f;
+__device__ __forceinline__ float final_lse(float M, float Z) {
+  return (M + __builtin_amdgcn_logf(Z)) * kLn2;
+}
+
 }  // namespace vd

@@ -53,13 +53,14 @@ def fill_pool(attn: VdAttn, call: W.Call, k_pool: torch.Tensor, v_pool: torch.Te
 
 def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
               hint_extra_q: int = 0, hint_extra_ctx: int = 0, append: bool = False,
-              shared_pages=None) -> DeviceCall:
+              shared_pages=None, lse: bool = False) -> DeviceCall:
     """Device copy of ``call``.  Pools start as bf16 NaN (``poison``) or zero,
     then receive every valid slot; host hints are the call's true maxima plus
     the given extras.  With ``append``, this call's own tokens are not written
     to the pool but handed to the batch (k_new, v_new: the K/V of the query
     rows), for the library to write before attention.  ``shared_pages`` is
-    set when some page is read by several requests (or as given)."""
+    set when some page is read by several requests (or as given).  With
+    ``lse`` the batch carries a NaN-filled [T, Hq] float32 log-sum-exp output."""
     fill = int(np.int16(np.uint16(W.BF16_QNAN).view(np.int16))) if poison else 0
     k_pool = attn.new_pool(call.num_pages, device)
     v_pool = attn.new_pool(call.num_pages, device)
@@ -70,6 +71,9 @@ def to_device(attn: VdAttn, call: W.Call, device="cuda", poison: bool = True,
     if append:
         kn, vn = call.query_kv()
         extra = dict(k_new=bf16_tensor(kn, device), v_new=bf16_tensor(vn, device))
+    if lse:
+        extra["lse"] = torch.full((call.total_q_tokens, call.shape.num_q_heads), float("nan"),
+                                  dtype=torch.float32, device=device)
     batch = Batch(
         q=bf16_tensor(call.q_bits(), device),
         cu_q_lens=torch.from_numpy(call.cu_q_lens).to(device),

@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(HERE, "libvdattn.so")
 HEADER = os.path.join(ROOT, "include", "vdattn.h")
 
 VD_OK = 0
-VD_ABI_VERSION = 3
+VD_ABI_VERSION = 4
 VD_DTYPE_BF16 = 1
 TILE_KEYS = 64
 SPLIT_KEYS = 512
@@ -52,7 +52,7 @@ class _Batch(ctypes.Structure):
                 ("v_pool", ctypes.c_void_p), ("num_pages", ctypes.c_int64),
                 ("max_q_len", ctypes.c_int32), ("max_context_len", ctypes.c_int32),
                 ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p),
-                ("shared_pages", ctypes.c_int32)]
+                ("shared_pages", ctypes.c_int32), ("lse", ctypes.c_void_p)]
 
 
 _lib = None
@@ -151,6 +151,8 @@ class Batch:
     v_new: Optional[torch.Tensor] = None  # [T, Hkv, D] bf16
     # host hint: some pages are read by several requests (keeps K/V cached)
     shared_pages: bool = False
+    # optional output: [T, Hq] float32 log-sum-exp of each row's visible scaled scores
+    lse: Optional[torch.Tensor] = None
 
 
 class VdAttn:
@@ -227,10 +229,12 @@ class VdAttn:
             per = self.num_kv_heads * self.head_dim
             _need(b.k_new, "k_new", torch.bfloat16, T * per)
             _need(b.v_new, "v_new", torch.bfloat16, T * per)
+        if b.lse is not None:
+            _need(b.lse, "lse", torch.float32, T * self.num_q_heads)
         return _Batch(B, T, _ptr(b.q), _ptr(b.cu_q_lens), _ptr(b.context_lens),
                       _ptr(b.page_table), stride, _ptr(b.k_pool), _ptr(b.v_pool),
                       int(b.num_pages), int(b.max_q_len), int(b.max_context_len),
-                      _ptr(b.k_new), _ptr(b.v_new), int(bool(b.shared_pages)))
+                      _ptr(b.k_new), _ptr(b.v_new), int(bool(b.shared_pages)), _ptr(b.lse))
 
     def _ws(self, b: Batch, workspace):
         need = self.workspace_size(int(b.context_lens.numel()), b.max_q_len, b.max_context_len)

@@ -39,12 +39,13 @@ def handle(shape: W.Shape) -> VdAttn:
 
 
 def gpu_run(call: W.Call, poison: bool = True, stream=None, workspace_fill=None,
-            prepared=None, **kw) -> np.ndarray:
+            prepared=None, with_lse: bool = False, **kw):
     """Output bits (uint16 [T, Hq, D]) of one vd_attn_forward call (or, with
     prepared = "forward" / "phases" / "timed", of a prepared call run whole, phase
-    by phase, or phase by phase with the kernels' dispatches recording events)."""
+    by phase, or phase by phase with the kernels' dispatches recording events).
+    With ``with_lse``: (output bits, log-sum-exp float32 [T, Hq])."""
     attn = handle(call.shape)
-    dc = S.to_device(attn, call, poison=poison, **kw)
+    dc = S.to_device(attn, call, poison=poison, lse=with_lse, **kw)
     ws = attn.new_workspace(call.num_seqs, dc.batch.max_q_len, dc.batch.max_context_len)
     if workspace_fill is not None:
         ws.view(torch.int8).fill_(workspace_fill)
@@ -75,16 +76,19 @@ def gpu_run(call: W.Call, poison: bool = True, stream=None, workspace_fill=None,
             attn.forward(dc.batch, out=out, workspace=ws, stream=stream)
         stream.synchronize()
     torch.cuda.synchronize()
+    if with_lse:
+        return S.bits_of(out), dc.batch.lse.cpu().numpy()
     return S.bits_of(out)
 
 
-def oracle_run(call: W.Call, rows=None) -> np.ndarray:
+def oracle_run(call: W.Call, rows=None, with_lse: bool = False):
     sh = call.shape
     kp, vp = call.std_pool()
     return oracle.paged_attention(call.q_bits(), call.cu_q_lens, call.context_lens,
                                   call.page_table, kp, vp, num_q_heads=sh.num_q_heads,
                                   num_kv_heads=sh.num_kv_heads, head_dim=sh.head_dim,
-                                  page_size=sh.page_size, window=sh.window, rows=rows)
+                                  page_size=sh.page_size, window=sh.window, rows=rows,
+                                  with_lse=with_lse)
 
 
 def by_position(call: W.Call, out: np.ndarray):

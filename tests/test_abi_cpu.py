@@ -47,9 +47,9 @@ def test_create_supported_and_destroy(lib):
 @pytest.mark.parametrize("kw,code", [
     (dict(head_dim=96), -2), (dict(head_dim=256), -2), (dict(page_size=32), -2),
     (dict(dtype=2), -2), (dict(num_q_heads=12, num_kv_heads=8), -2),
-    (dict(num_q_heads=64, num_kv_heads=1), -2), (dict(abi_version=4), -1),
+    (dict(num_q_heads=64, num_kv_heads=1), -2), (dict(abi_version=5), -1),
     (dict(num_kv_heads=0), -1), (dict(softmax_scale=float("nan")), -1), (dict(window=-1), -1),
-    (dict(abi_version=1), -1), (dict(abi_version=2), -1),
+    (dict(abi_version=1), -1), (dict(abi_version=2), -1), (dict(abi_version=3), -1),
 ])
 def test_create_rejects(lib, kw, code):
     rc, h = _create(lib, **kw)
