@@ -1,4 +1,5 @@
-"""Plain CPU oracle for paged causal attention -- TEST INFRASTRUCTURE ONLY.
+"""Plain CPU oracle for paged causal attention and for the linear layer --
+TEST INFRASTRUCTURE ONLY.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product path (the HIP library and
@@ -60,6 +61,10 @@ def bind(path: str):
         ctypes.c_int, ctypes.c_double, ctypes.c_int, P, P, P, P, ctypes.c_int, P, P,
         ctypes.c_int64, P, P, P, ctypes.c_int]
     lib.vdo_default_threads.restype = ctypes.c_int
+    if hasattr(lib, "vdo_linear"):
+        lib.vdo_linear.restype = ctypes.c_int
+        lib.vdo_linear.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.c_int, P, ctypes.c_int64,
+                                   P, ctypes.c_int64, P, ctypes.c_int]
     return lib
 
 
@@ -141,3 +146,25 @@ def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_
         raise ValueError("oracle rejected the call: %s (%d)" % (ERRORS.get(rc, "?"), rc))
     return (out, lse) if with_lse else out
 
+
+def linear(a_bits, b_bits, *, k=None, threads=0, lib=None):
+    """Exact (fp64) linear layer, c = a . b^T (the matmul contract of the
+    paper's Section 5.4, Fig. 3).
+
+    a_bits: uint16 [M, lda] bf16 bit patterns (activations; the first k
+            columns are used, k defaults to lda).
+    b_bits: uint16 [N, ldb] bf16 bit patterns (weights, one row per output
+            column; the first k columns are used).
+    Returns float64 [M, N]."""
+    lib = _load() if lib is None else lib
+    a, ap = _c(a_bits, np.uint16)
+    b, bp = _c(b_bits, np.uint16)
+    assert a.ndim == 2 and b.ndim == 2
+    M, lda = a.shape
+    N, ldb = b.shape
+    K = lda if k is None else int(k)
+    c = np.full((M, N), np.nan, np.float64)
+    rc = lib.vdo_linear(M, N, K, ap, lda, bp, ldb, c.ctypes.data_as(ctypes.c_void_p), int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the linear call: %s (%d)" % (ERRORS.get(rc, "?"), rc))
+    return c

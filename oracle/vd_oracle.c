@@ -42,6 +42,12 @@
  * Every sum runs in ascending index order in double precision.  No blocking,
  * no online softmax, no splitting: the definition written out.
  *
+ * Linear layer (the matmul contract of Section 5.4, Fig. 3: the output row
+ * of a token depends only on that token's input row and the weights):
+ *       c[m][n] = sum_k a[m][k] * b[n][k]      for k = 0..K-1
+ *   with a the activations [M][K] and b the weights [N][K] (one row per output
+ *   column, as a linear layer stores them), in double, k ascending.
+ *
  * Error behaviour: returns 0 on success, a negative code on invalid input
  * (nothing is written to `out` for a rejected call).
  */
@@ -242,3 +248,67 @@ int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
 
 /* Number of host threads the oracle uses when asked for "all cores". */
 int vdo_default_threads(void) { return (int)sysconf(_SC_NPROCESSORS_ONLN); }
+
+/* ------------------------------------------------------------------------ */
+/* Linear layer: c[m][n] = sum_k a[m][k] * b[n][k], k ascending, in double.
+ * a: M rows of lda bf16 values (the first K used), b: N rows of ldb bf16
+ * values (the first K used), c: M rows of N doubles.  Returns 0, or
+ * VDO_ERR_ARG for an invalid size or stride. */
+typedef struct {
+  int64_t M;
+  int N, K;
+  const uint16_t *a, *b;
+  int64_t lda, ldb;
+  double *c;
+  int64_t next_row;
+  pthread_mutex_t lock;
+} lin_job_t;
+
+static void *lin_worker(void *arg) {
+  lin_job_t *J = (lin_job_t *)arg;
+  for (;;) {
+    pthread_mutex_lock(&J->lock);
+    const int64_t m = J->next_row++;
+    pthread_mutex_unlock(&J->lock);
+    if (m >= J->M) break;
+    const uint16_t *arow = J->a + m * J->lda;
+    double *crow = J->c + m * (int64_t)J->N;
+    for (int n = 0; n < J->N; ++n) {
+      const uint16_t *brow = J->b + (int64_t)n * J->ldb;
+      double acc = 0.0;
+      for (int k = 0; k < J->K; ++k)
+        acc += bf16_to_double(arow[k]) * bf16_to_double(brow[k]);
+      crow[n] = acc;
+    }
+  }
+  return NULL;
+}
+
+int vdo_linear(int64_t M, int N, int K, const uint16_t *a, int64_t lda,
+               const uint16_t *b, int64_t ldb, double *c, int num_threads) {
+  if (M < 0 || N < 0 || K < 0 || lda < K || ldb < K) return VDO_ERR_ARG;
+  if (M == 0 || N == 0) return VDO_OK;
+  if (!a || !b || !c) return VDO_ERR_ARG;
+  lin_job_t J;
+  memset(&J, 0, sizeof J);
+  J.M = M;
+  J.N = N;
+  J.K = K;
+  J.a = a;
+  J.b = b;
+  J.lda = lda;
+  J.ldb = ldb;
+  J.c = c;
+  if (num_threads <= 0) num_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);
+  if (num_threads < 1) num_threads = 1;
+  pthread_mutex_init(&J.lock, NULL);
+  pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)num_threads);
+  if (!th) return VDO_ERR_NOMEM;
+  int started = 0;
+  for (int i = 0; i < num_threads; ++i)
+    if (pthread_create(&th[i], NULL, lin_worker, &J) == 0) ++started;
+  for (int i = 0; i < started; ++i) pthread_join(th[i], NULL);
+  free(th);
+  pthread_mutex_destroy(&J.lock);
+  return started ? VDO_OK : VDO_ERR_NOMEM;
+}

@@ -374,10 +374,81 @@ def pin_lse_closed_forms(lib):
             np.testing.assert_allclose(np.exp(sc - lse[i, h]).sum(), 1.0, rtol=0, atol=1e-12)
 
 
+# ---------------------------------------------------------------------------
+# linear layer (the matmul contract of Section 5.4, Fig. 3): c = a . b^T
+# ---------------------------------------------------------------------------
+def _bf16_ints(rng, shape, lo=-8, hi=8):
+    """bf16 bit patterns of small integers (exact in bf16), and the integers."""
+    vals = rng.integers(lo, hi + 1, size=shape)
+    return W.bf16_bits(vals.astype(np.float32)), vals.astype(np.int64)
+
+
+def pin_linear_integer_exact(lib):
+    """Small-integer inputs make every product and every partial sum exact in
+    fp64, so the oracle equals numpy's int64 matmul a @ b^T; the shapes are
+    not square and the operands not symmetric, so a transposed operand, a
+    dropped or repeated term or a wrong index fails."""
+    rng = np.random.default_rng(31)
+    for M, N, K in [(5, 7, 3), (1, 9, 33), (13, 2, 64), (4, 4, 4)]:
+        ab, ai = _bf16_ints(rng, (M, K))
+        bb, bi = _bf16_ints(rng, (N, K))
+        c = oracle.linear(ab, bb, lib=lib)
+        assert np.array_equal(c, (ai @ bi.T).astype(np.float64)), (M, N, K)
+
+
+def pin_linear_one_hot(lib):
+    """A one-hot activation row (a single 1 at column k_m) selects one column
+    of the weights: c[m, n] = b[n, k_m] bit for bit (random bf16 weights)."""
+    rng = np.random.default_rng(32)
+    M, N, K = 6, 11, 40
+    hot = rng.integers(0, K, size=M)
+    a = np.zeros((M, K), np.float32)
+    a[np.arange(M), hot] = 1.0
+    bb = W.normal_bf16(rng, (N, K))
+    c = oracle.linear(W.bf16_bits(a), bb, lib=lib)
+    assert np.array_equal(c, f64(bb)[:, hot].T)
+
+
+def pin_linear_strided(lib):
+    """Only the first k columns of a and b are read: with NaN in the columns
+    past k (a row stride larger than k) the result equals the contiguous one."""
+    rng = np.random.default_rng(33)
+    M, N, K = 7, 5, 24
+    a = W.normal_bf16(rng, (M, K))
+    b = W.normal_bf16(rng, (N, K))
+    a_pad = np.full((M, K + 9), W.BF16_QNAN, np.uint16)
+    b_pad = np.full((N, K + 3), W.BF16_QNAN, np.uint16)
+    a_pad[:, :K] = a
+    b_pad[:, :K] = b
+    c = oracle.linear(a_pad, b_pad, k=K, lib=lib)
+    assert np.array_equal(c, oracle.linear(a, b, lib=lib))
+
+
+def pin_linear_fsum_bound(lib):
+    """Random bf16 inputs: every bf16 x bf16 product is exact in fp64, so the
+    ascending fp64 sum lies within K * 2^-53 * sum |a_k b_k| of the exactly
+    rounded sum of the same products (math.fsum)."""
+    import math
+
+    rng = np.random.default_rng(34)
+    M, N, K = 3, 4, 300
+    a = W.normal_bf16(rng, (M, K))
+    b = W.normal_bf16(rng, (N, K))
+    c = oracle.linear(a, b, lib=lib)
+    af, bf = f64(a), f64(b)
+    for m in range(M):
+        for n in range(N):
+            prods = [af[m, k] * bf[n, k] for k in range(K)]
+            bound = K * 2.0 ** -53 * sum(abs(x) for x in prods)
+            assert abs(c[m, n] - math.fsum(prods)) <= bound, (m, n)
+
+
 ALL_PINS = [pin_sdpa_prefill, pin_sdpa_chunk_offset, pin_sdpa_scale, pin_scipy_softmax_dense,
             pin_single_key, pin_zero_query_mean, pin_identical_keys_mean, pin_dominant_key,
             pin_fig4_example, pin_invariances, pin_sdpa_window, pin_window_one_key,
-            pin_window_zero_query_mean, pin_window_limits, pin_lse_scipy, pin_lse_closed_forms]
+            pin_window_zero_query_mean, pin_window_limits, pin_lse_scipy, pin_lse_closed_forms,
+            pin_linear_integer_exact, pin_linear_one_hot, pin_linear_strided,
+            pin_linear_fsum_bound]
 
 
 if __name__ == "__main__":

@@ -83,6 +83,14 @@ def test_empty_batch():
     assert out.shape == (0, 4, 64)
 
 
+def test_linear_rejects_bad_sizes():
+    a = np.zeros((2, 8), np.uint16)
+    b = np.zeros((3, 8), np.uint16)
+    with pytest.raises(ValueError):
+        oracle.linear(a, b, k=9)  # k beyond the row stride
+    assert oracle.linear(a[:0], b).shape == (0, 3)
+
+
 # ---------------------------------------------------------------------------
 # planted mistakes: every mutant must fail at least one pin
 # ---------------------------------------------------------------------------
@@ -108,6 +116,16 @@ MUTANTS = {
     "lse_sign": ("J->lse[t * J->hq + h] = mx + log(denom);", "J->lse[t * J->hq + h] = mx - log(denom);"),
     "window_from_n": ("p - J->window + 1 > 0) ? p - J->window + 1 : 0;",
                       "n - J->window + 1 > 0) ? n - J->window + 1 : 0;"),
+    # linear layer
+    "linear_transposed_weights": ("acc += bf16_to_double(arow[k]) * bf16_to_double(brow[k]);",
+                                  "acc += bf16_to_double(arow[k]) * bf16_to_double(J->b[(int64_t)(k % J->N) * J->ldb + n % J->K]);"),
+    "linear_drops_last_k": ("for (int k = 0; k < J->K; ++k)", "for (int k = 0; k < J->K - 1; ++k)"),
+    "linear_ignores_stride": ("const uint16_t *arow = J->a + m * J->lda;",
+                              "const uint16_t *arow = J->a + m * J->K;"),
+    "linear_previous_row": ("const uint16_t *arow = J->a + m * J->lda;",
+                            "const uint16_t *arow = J->a + (m > 0 ? m - 1 : 0) * J->lda;"),
+    "linear_sign": ("acc += bf16_to_double(arow[k]) * bf16_to_double(brow[k]);",
+                    "acc -= bf16_to_double(arow[k]) * bf16_to_double(brow[k]);"),
 }
 
 
