@@ -72,7 +72,8 @@ def measured_traffic(kernel: str, workload: str):
     with open(path) as f:
         d = json.load(f)
     csrc = os.path.join(ROOT, "paper_2609_38981_amd", "csrc")
-    src = b"".join(open(os.path.join(csrc, n), "rb").read() for n in ("vd_attn.hip", "vd_cas.hpp"))
+    src = b"".join(open(os.path.join(csrc, n), "rb").read()
+                   for n in ("vd_attn.hip", "vd_cas.hpp", "vd_hw.hpp"))
     if d.get("source_sha256") != hashlib.sha256(src).hexdigest():
         return None
     if d.get("kernel") != kernel or d.get("workload") != workload:
@@ -129,12 +130,112 @@ def cpu_baseline(call, min_seconds: float = 10.0, max_requests: int = 64):
                                           sub.kv_bytes() / 1e6, reps, sec)}
 
 
+# The batch-invariant linear layer (vd_linear): (M tokens, N outputs, K inputs)
+LINEAR_WORKLOADS = {
+    "linear8b": ((4096, 6144, 4096),
+                 "Llama-3-8B QKV projection: 4096 tokens, 4096 -> 6144 (q 4096, k 1024, v 1024), "
+                 "bf16 activations and weights, fp32 accumulation"),
+}
+
+
+def linear_cpu_baseline(a_bits, b_bits, min_seconds: float = 10.0):
+    """The oracle (fp64 plain loops) on a bounded sample of the same layer: the
+    first rows of the activations, repeated until at least ``min_seconds``."""
+    import oracle
+
+    M, K = a_bits.shape
+    N = b_bits.shape[0]
+    rows = max(1, min(M, int(4e9 // (2 * N * K))))  # ~4 GFLOP of work per repetition
+    threads = host_threads()
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.linear(a_bits[:rows], b_bits, threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or reps >= 1000:
+            break
+    sec = el / reps
+    return {"value": round(2.0 * rows * N * K / sec / 1e12, 6), "unit": "TFLOP/s",
+            "cores": threads, "kind": "oracle",
+            "sample": "%d of %d rows (%d x %d x %d), %d repetitions, %.2f s per repetition"
+                      % (rows, M, rows, N, K, reps, sec)}
+
+
+def bench_linear(args):
+    """One step = one vd_linear call over the whole layer (inputs resident in
+    HBM, R replicas cycled); the kernel is the whole step."""
+    import torch
+
+    from paper_2609_38981_amd import staging as S
+    from paper_2609_38981_amd import vdattn as V
+    from paper_2609_38981_amd import workloads as W
+
+    (M, N, K), desc = LINEAR_WORKLOADS[args.workload]
+    rng = W.rng_for(7, 1)
+    a_bits, b_bits = W.normal_bf16(rng, (M, K)), W.normal_bf16(rng, (N, K))
+    reps = []
+    for _ in range(max(args.replicas, 1)):
+        a, b = S.bf16_tensor(a_bits, "cuda"), S.bf16_tensor(b_bits, "cuda")
+        reps.append((a, b, torch.empty((M, N), dtype=torch.bfloat16, device="cuda")))
+    stream = torch.cuda.current_stream()
+    for i in range(args.warmup):
+        V.linear(*reps[i % len(reps)])
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        a, b, c = reps[i % len(reps)]
+        evs[i][0].record(stream)
+        V.linear(a, b, c)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    k_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    flop = 2.0 * M * N * K
+    ach = flop / (k_ms * 1e-3) / 1e12
+    # context: the vendor library GEMM on the same shapes (not batch-invariant in general)
+    a, b, c = reps[0]
+    bt = b.t()
+    for _ in range(3):
+        torch.matmul(a, bt, out=c)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(20):
+        torch.matmul(a, bt, out=c)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    lib_ms = e0.elapsed_time(e1) / 20
+    log("linear %s: %.4f ms/step, kernel %.4f ms = %.1f TFLOP/s; torch.matmul %.4f ms"
+        % (args.workload, ms, k_ms, ach, lib_ms))
+    res = {
+        "metric": "batch-invariant linear TFLOP/s (bf16, fp32 accumulation)",
+        "value": round(flop / (ms * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": desc, "M": M, "N": N, "K": K, "replicas": len(reps)},
+        "roofline": {"kernel": "linear_kernel", "bound": "mfma", "achieved": round(ach, 2),
+                     "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                     "frac": round(ach / MFMA_BF16_PEAK_TFS, 4), "traffic": None,
+                     "avg_ms": round(k_ms, 5), "timed_launches": args.steps,
+                     "algorithmic_flop": int(flop)},
+        "torch_matmul_tflops": round(flop / (lib_ms * 1e-3) / 1e12, 2),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle baseline")
+        res["cpu_baseline"] = linear_cpu_baseline(a_bits, b_bits)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="decode8b", choices=sorted(workloads()))
+    ap.add_argument("--workload", default="decode8b",
+                    choices=sorted(workloads()) + sorted(LINEAR_WORKLOADS))
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--time-every", type=int, default=4,
@@ -155,6 +256,8 @@ def main():
     from paper_2609_38981_amd import staging as S
 
     torch.cuda.set_device(0)
+    if args.workload in LINEAR_WORKLOADS:
+        return bench_linear(args)
     make, desc = workloads()[args.workload]
     t0 = time.perf_counter()
     call = make()

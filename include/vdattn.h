@@ -215,6 +215,25 @@ int vd_kv_write(const vd_attn* h, const void* k_new, const void* v_new,
                 const int64_t* slot_mapping, int64_t num_tokens, void* k_pool, void* v_pool,
                 int64_t num_pages, hipStream_t stream);
 
+/* Batch-invariant linear layer (the matmul contract of Section 5.4, Fig. 3: the output
+ * row of a token depends only on that token's input row and on the weights):
+ *   c[m][n] = bf16_RNE( sum_k a[m][k] * b[n][k] )   for 0 <= m < M, 0 <= n < N
+ * a: device [M rows of lda] bf16 activations (the first K values of a row used);
+ * b: device [N rows of ldb] bf16 weights, one row per output feature (the layout a
+ *    linear layer stores, [out_features, in_features]); the first K values used;
+ * c: device [M rows of ldc] bf16 output (the first N values of a row written).
+ * Each output element is one fp32 accumulation chain of v_mfma_f32_16x16x32_bf16 over K
+ * in ascending 32-wide chunks starting from +0, cast to bf16 round-to-nearest-even: row m
+ * of c is bit-identical for any M, any position of the row in a, and any strides.  The
+ * tiling is fixed (it depends on nothing but the build); there is no split over K.
+ * Requirements (else VD_ERR_UNSUPPORTED for K, VD_ERR_INVALID_ARG otherwise): K a multiple
+ * of 64; when K > 0, lda, ldb >= K and multiples of 8 with a and b 16-byte aligned (K = 0:
+ * a and b are not read and every output is +0); ldc >= N; c 2-byte aligned; M, N, K >= 0
+ * (M = 0 or N = 0: nothing to do).  Launches on `stream` and
+ * returns without waiting; allocates nothing.  Strides are in elements. */
+int vd_linear(const void* a, int64_t lda, const void* b, int64_t ldb, void* c, int64_t ldc,
+              int64_t M, int32_t N, int32_t K, hipStream_t stream);
+
 /* Static description of a status code (never NULL). */
 const char* vd_status_string(int status);
 

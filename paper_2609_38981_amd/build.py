@@ -1,4 +1,5 @@
-"""Builds libvdattn.so (HIP, gfx950) in-tree with hipcc."""
+"""Builds libvdattn.so (HIP, gfx950: paged attention and the linear layer)
+in-tree with hipcc."""
 from __future__ import annotations
 
 import os
@@ -8,7 +9,9 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "vd_attn.hip")
-DEPS = [SRC, os.path.join(HERE, "csrc", "vd_cas.hpp"), os.path.join(ROOT, "include", "vdattn.h")]
+SRC_LINEAR = os.path.join(HERE, "csrc", "vd_linear.hip")
+DEPS = [SRC, SRC_LINEAR, os.path.join(HERE, "csrc", "vd_cas.hpp"), os.path.join(HERE, "csrc", "vd_hw.hpp"),
+        os.path.join(ROOT, "include", "vdattn.h")]
 LIB = os.path.join(HERE, "libvdattn.so")
 
 HIPCC_FLAGS = [
@@ -37,7 +40,7 @@ def build(force: bool = True, verbose: bool = False) -> str:
             os.path.getmtime(LIB) >= os.path.getmtime(d) for d in DEPS):
         return LIB
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), SRC, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), SRC, SRC_LINEAR, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if verbose or res.returncode != 0:
         # hipcc's host pass reports the device-only feature flag as unknown

@@ -32,6 +32,7 @@
 
 #include "../../include/vdattn.h"
 #include "vd_cas.hpp"
+#include "vd_hw.hpp"
 
 using namespace vd;
 
@@ -89,15 +90,6 @@ __device__ __forceinline__ Req make_req(const Params& P, int q0, int q1, int n) 
 
 __device__ __forceinline__ Req load_req(const Params& P, int r) {
   return make_req(P, P.cu[r], P.cu[r + 1], P.ctx[r]);
-}
-
-__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
-
-// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
 
@@ -472,23 +464,6 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
 // ---------------------------------------------------------------------------
 // split kernel
 // ---------------------------------------------------------------------------
-// Direct global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
-// byte address m0val + 16 l.  Issued as inline assembly so that the compiler
-// does not make every later LDS read wait for all such copies; the kernel
-// waits for them itself with wait_vmcnt.  M0 is saved and restored.
-__device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0val) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(src), "s"(m0val)
-      : "memory");
-}
-
 // Issue the loads of one tile's K (resp. V) operands.  Every lane loads from
 // a valid page block (a page id that is out of range or past n reads block 0
 // instead), so the load sequence is the same on every tile; the values that
@@ -1155,14 +1130,6 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
 #define VD_CHUNK_STAGES 2
 #endif
 constexpr int kChunkStages = VD_CHUNK_STAGES;
-
-// Workgroup barrier that orders LDS accesses only (global memory operations
-// in flight are not waited for).
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 // Two workgroups per CU (waves_per_eu 2: at most 256 registers per lane, and
 // two LDS rings of kChunkStages tiles): while one wavefront of a SIMD waits on

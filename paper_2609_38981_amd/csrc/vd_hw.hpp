@@ -1,0 +1,45 @@
+// vd_hw.hpp -- gfx950 helpers shared by the library's kernels: wave-uniform
+// values, vector-memory wait counts, direct global-to-LDS copies and an
+// LDS-only workgroup barrier.  No arithmetic of any result lives here.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vd {
+
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Direct global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
+// byte address m0val + 16 l.  Issued as inline assembly so that the compiler
+// does not make every later LDS read wait for all such copies; the kernel
+// waits for them itself with wait_vmcnt.  M0 is saved and restored.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0val) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(m0val)
+      : "memory");
+}
+
+// Workgroup barrier that orders LDS accesses only (global memory operations
+// in flight are not waited for).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+}  // namespace vd

@@ -1,0 +1,180 @@
+// vd_linear.hip -- the batch-invariant linear layer of libvdattn.so (gfx950).
+//
+// c[m][n] = bf16_RNE( sum_k a[m][k] * b[n][k] ): the matmul contract of the
+// paper's Section 5.4 (Fig. 3): the output row of a token depends only on that
+// token's input row and on the weights, however many rows the call holds and
+// wherever the row sits among them.
+//
+// Canonical arithmetic (one chain per output element, fixed by K alone):
+//   acc = +0 (fp32); for k0 = 0, 32, 64, ... < K (ascending):
+//     acc = v_mfma_f32_16x16x32_bf16(a[m][k0 .. k0+31], b[n][k0 .. k0+31], acc)
+//   c[m][n] = bf16 round-to-nearest-even of acc.
+// The result of one MFMA output cell depends only on its own row of the A
+// operand, its own column of the B operand and its accumulator cell (the
+// property vd_cas.hpp relies on), so neither the tiling, nor the workgroup that
+// computes a row, nor the other rows of the call reach its bits; only K (the
+// chain length and order) does, and there is no split over K.
+//
+// Launch: one workgroup of 4 wavefronts per 128 x 128 output tile, each
+// wavefront a 64 x 64 quarter (4 x 4 MFMA blocks of 16 x 16).  K advances in
+// steps of 64 through a 2-stage LDS ring of A and B tiles (128 rows x 64
+// values each) filled by direct global-to-LDS copies; the 16-byte chunks of
+// each 128-byte LDS row are XOR-swizzled by the row so that the 16 rows one
+// operand read touches fall in different banks.  Tiles are taken in groups of
+// 4 row tiles sweeping the column tiles, and each XCD (workgroup id mod 8)
+// takes a contiguous range of that order, so the A and B panels of its
+// workgroups are shared in its L2.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/vdattn.h"
+#include "vd_cas.hpp"
+#include "vd_hw.hpp"
+
+using namespace vd;
+
+namespace {
+
+constexpr int kBM = 128;   // rows of a (tokens) per workgroup tile
+constexpr int kBN = 128;   // rows of b (output features) per workgroup tile
+constexpr int kBK = 64;    // K per step (two 32-wide MFMA chunks)
+constexpr int kGroupM = 4; // row tiles per group of the tile order
+constexpr int kTileBytes = kBM * kBK * 2;            // one staged A (or B) tile: 16 KB
+constexpr int kStageBytes = 2 * kTileBytes;          // A then B
+constexpr int kLinLds = 2 * kStageBytes;             // 2-stage ring: 64 KB
+constexpr int kCopies = kTileBytes / 1024 / 4;       // 1 KB copies per wavefront per tile
+
+// LDS byte offset of 16-byte chunk ch (0..7) of row r in a staged tile.
+__device__ __forceinline__ int swz(int r, int ch) { return r * 128 + ((ch ^ (r & 7)) << 4); }
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void linear_kernel(
+    const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, uint16_t* c, int64_t ldc,
+    int64_t M, int N, int K, int tiles_m, int tiles_n) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  const int wave = uni(threadIdx.x >> 6);
+  const int lane = __lane_id();
+  // tile order: groups of kGroupM row tiles, each sweeping the column tiles
+  // (row tile fastest); XCD x takes the x-th contiguous eighth of the order
+  const int64_t total = (int64_t)tiles_m * tiles_n;
+  const int64_t per_xcd = (total + 7) / 8;
+  const int64_t jx = blockIdx.x / 8;
+  if (jx >= per_xcd) return;
+  const int64_t i = (int64_t)(blockIdx.x % 8) * per_xcd + jx;
+  if (i >= total) return;
+  const int64_t group = i / ((int64_t)kGroupM * tiles_n);
+  const int64_t first_m = group * kGroupM;
+  const int size_m = (int)((tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM);
+  const int in_group = (int)(i - group * (int64_t)kGroupM * tiles_n);
+  const int64_t m0 = (first_m + in_group % size_m) * kBM;
+  const int n0 = (in_group / size_m) * kBN;
+
+  // Copies: wavefront w moves rows 32 w .. 32 w + 31 of each staged tile, 8
+  // rows per 1 KB copy; lane l of copy j carries row 32 w + 8 j + l / 8,
+  // chunk (l % 8) ^ (l / 8) -- its LDS slot is 16 l bytes into the copy, which
+  // is chunk l % 8 of that row after the swizzle.  Rows past M (or N) repeat
+  // the last row: in bounds, and never stored.
+  const int cch = (lane & 7) ^ (lane >> 3);
+  const uint16_t* asrc[kCopies];
+  const uint16_t* bsrc[kCopies];
+#pragma unroll
+  for (int j = 0; j < kCopies; ++j) {
+    const int r = 32 * wave + 8 * j + (lane >> 3);
+    const int64_t ra = m0 + r < M ? m0 + r : M - 1;
+    const int rb = n0 + r < N ? n0 + r : N - 1;
+    asrc[j] = a + ra * lda + 8 * cch;
+    bsrc[j] = b + (int64_t)rb * ldb + 8 * cch;
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+  auto fetch = [&](int step, int buf) {
+    const int k0 = step * kBK;
+    const uint32_t st = lds0 + buf * kStageBytes + wave * (kCopies * 1024);
+#pragma unroll
+    for (int j = 0; j < kCopies; ++j) lds_dma16(asrc[j] + k0, uni((int)(st + 1024 * j)));
+#pragma unroll
+    for (int j = 0; j < kCopies; ++j)
+      lds_dma16(bsrc[j] + k0, uni((int)(st + kTileBytes + 1024 * j)));
+  };
+
+  // this wavefront's quarter: rows wm .. wm + 63, columns wn .. wn + 63
+  const int wm = 64 * (wave >> 1), wn = 64 * (wave & 1);
+  const int col = lane & 15, grp = lane >> 4;
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int steps = K / kBK;
+  if (steps > 0) fetch(0, 0);
+  for (int t = 0; t < steps; ++t) {
+    if (t + 1 < steps) {
+      fetch(t + 1, (t + 1) & 1);
+      wait_vmcnt<2 * kCopies>();  // this wavefront's copies of step t have landed
+    } else {
+      wait_vmcnt<0>();
+    }
+    lds_barrier();  // every wavefront's copies of step t have landed
+    const uint16_t* TA = lds + (t & 1) * (kStageBytes / 2);
+    const uint16_t* TB = TA + kTileBytes / 2;
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      // operand of lane (col, grp): row col of the block, k = 32 kc + 8 grp .. + 7
+      u16x8 af[4], bf[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        af[x] = *reinterpret_cast<const u16x8*>(
+            reinterpret_cast<const char*>(TA) + swz(wm + 16 * x + col, 4 * kc + grp));
+        bf[x] = *reinterpret_cast<const u16x8*>(
+            reinterpret_cast<const char*>(TB) + swz(wn + 16 * x + col, 4 * kc + grp));
+      }
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = mfma(af[x], bf[y], acc[x][y]);
+    }
+    lds_barrier();  // every wavefront is done with stage t & 1 before it is refilled
+  }
+
+  // accumulator cell i of block (x, y) in lane (col, grp): row 16 x + 4 grp + i, column 16 y + col
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = m0 + wm + 16 * x + 4 * grp + i;
+      if (row >= M) continue;
+#pragma unroll
+      for (int y = 0; y < 4; ++y) {
+        const int cn = n0 + wn + 16 * y + col;
+        if (cn < N) c[row * ldc + cn] = bf16_rne(acc[x][y][i]);
+      }
+    }
+}
+
+}  // namespace
+
+extern "C" int vd_linear(const void* a, int64_t lda, const void* b, int64_t ldb, void* c,
+                         int64_t ldc, int64_t M, int32_t N, int32_t K, hipStream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return VD_ERR_INVALID_ARG;
+  if (M == 0 || N == 0) return VD_OK;
+  if (!c || ldc < N || (uintptr_t)c % 2 != 0) return VD_ERR_INVALID_ARG;
+  if (K % kBK != 0) return VD_ERR_UNSUPPORTED;
+  // a and b are read only when K > 0 (K = 0: every output is the empty sum, +0)
+  if (K > 0) {
+    if (!a || !b) return VD_ERR_INVALID_ARG;
+    if (lda < K || ldb < K || lda % 8 != 0 || ldb % 8 != 0) return VD_ERR_INVALID_ARG;
+    if (((uintptr_t)a | (uintptr_t)b) % 16 != 0) return VD_ERR_INVALID_ARG;
+  }
+  const int64_t tiles_m = (M + kBM - 1) / kBM, tiles_n = ((int64_t)N + kBN - 1) / kBN;
+  const int64_t total = tiles_m * tiles_n;
+  const int64_t blocks = (total + 7) / 8 * 8;
+  if (tiles_m > INT32_MAX || blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&linear_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+      kLinLds);
+  if (attr != hipSuccess) return VD_ERR_LAUNCH;
+  hipLaunchKernelGGL(linear_kernel, dim3((unsigned)blocks), dim3(256), kLinLds, stream,
+                     static_cast<const uint16_t*>(a), lda, static_cast<const uint16_t*>(b), ldb,
+                     static_cast<uint16_t*>(c), ldc, M, N, K, (int)tiles_m, (int)tiles_n);
+  return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH;
+}

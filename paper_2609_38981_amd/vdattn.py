@@ -83,6 +83,7 @@ def load_library(path: str = LIB_PATH):
                                          [P, ctypes.POINTER(_Batch), P, P, SZ, P, P, P]),
         "vd_pool_bytes": (ctypes.c_int, [P, I64, ctypes.POINTER(SZ)]),
         "vd_kv_write": (ctypes.c_int, [P, P, P, P, I64, P, P, I64, P]),
+        "vd_linear": (ctypes.c_int, [P, I64, P, I64, P, I64, I64, I32, I32, P]),
         "vd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "vd_attn_tiling": (ctypes.c_int, [P, ctypes.POINTER(I32), ctypes.POINTER(I32),
                                           ctypes.POINTER(I32)]),
@@ -368,3 +369,28 @@ class PreparedCall:
 
     def merge(self):
         self._run(self._merge, "vd_attn_forward_merge")
+
+
+def linear(a: torch.Tensor, b: torch.Tensor, out: Optional[torch.Tensor] = None,
+           stream=None) -> torch.Tensor:
+    """Batch-invariant linear layer (vd_linear): out = a @ b^T with a [M, K]
+    bf16 activations and b [N, K] bf16 weights, out [M, N] bf16; row m of the
+    output depends only on row m of a and on b.  Rows may be strided (the
+    last dimension contiguous)."""
+    lib = load_library()
+    for t, name in ((a, "a"), (b, "b")):
+        if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dtype != torch.bfloat16:
+            raise TypeError("%s must be a bf16 device tensor" % name)
+        if t.dim() != 2 or t.stride(1) != 1:
+            raise ValueError("%s must be 2-D with contiguous rows" % name)
+    M, K = a.shape
+    N, Kb = b.shape
+    if Kb != K:
+        raise ValueError("a is [M, %d] but b is [N, %d]" % (K, Kb))
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    if out.dtype != torch.bfloat16 or out.dim() != 2 or out.shape != (M, N) or out.stride(1) != 1:
+        raise ValueError("out must be bf16 [M, N] with contiguous rows")
+    _check(lib.vd_linear(a.data_ptr(), a.stride(0), b.data_ptr(), b.stride(0), out.data_ptr(),
+                         out.stride(0), M, N, K, _stream(stream)), "vd_linear")
+    return out
