@@ -36,17 +36,33 @@ using namespace vd;
 
 namespace {
 
-constexpr int kBM = 128;   // rows of a (tokens) per workgroup tile
-constexpr int kBN = 128;   // rows of b (output features) per workgroup tile
-constexpr int kBK = 64;    // K per step (two 32-wide MFMA chunks)
-constexpr int kGroupM = 4; // row tiles per group of the tile order
-constexpr int kTileBytes = kBM * kBK * 2;            // one staged A (or B) tile: 16 KB
-constexpr int kStageBytes = 2 * kTileBytes;          // A then B
-constexpr int kLinLds = 2 * kStageBytes;             // 2-stage ring: 64 KB
-constexpr int kCopies = kTileBytes / 1024 / 4;       // 1 KB copies per wavefront per tile
+// Tile configuration: each of the 4 wavefronts (2 x 2) computes kXB x kYB MFMA
+// blocks of 16 x 16; K advances kBK per step (kBK / 32 MFMA chunks).  On the
+// Llama-3-8B QKV shape, 4 x 4 blocks with 64-wide steps (two workgroups per
+// CU) ran faster than 4 x 8 or 8 x 4 blocks with 32- or 64-wide steps.
+constexpr int kXB = 4, kYB = 4, kBK = 64;
+constexpr int kBM = 2 * 16 * kXB;           // rows of a (tokens) per workgroup tile
+constexpr int kBN = 2 * 16 * kYB;           // rows of b (output features) per workgroup tile
+constexpr int kRowBytes = kBK * 2;          // one staged row of a tile
+constexpr int kChunks = kRowBytes / 16;     // 16-byte chunks per staged row
+constexpr int kRowsPerCopy = 1024 / kRowBytes;
+constexpr int kGroupM = 4;                  // row tiles per group of the tile order
+constexpr int kTileA = kBM * kRowBytes, kTileB = kBN * kRowBytes;
+constexpr int kStageBytes = kTileA + kTileB;
+constexpr int kLinLds = 2 * kStageBytes;    // 2-stage ring
+constexpr int kCopiesA = kTileA / 1024 / 4, kCopiesB = kTileB / 1024 / 4;  // per wavefront
+static_assert(kChunks == 4 || kChunks == 8, "staged rows of 64 or 128 bytes");
+static_assert(kCopiesA * 4096 == kTileA && kCopiesB * 4096 == kTileB, "copy split");
 
-// LDS byte offset of 16-byte chunk ch (0..7) of row r in a staged tile.
-__device__ __forceinline__ int swz(int r, int ch) { return r * 128 + ((ch ^ (r & 7)) << 4); }
+// Swizzle key of staged row r: chunk ch of the row sits in 16-byte slot
+// ch ^ key(r), so that 8 consecutive rows read at one chunk fill 8 distinct
+// 16-byte slots of a 128-byte bank window.
+__device__ __forceinline__ int swz_key(int r) {
+  return kChunks == 8 ? (r & 7) : ((r >> 1) & 3);
+}
+__device__ __forceinline__ int swz(int r, int ch) {
+  return r * kRowBytes + ((ch ^ swz_key(r)) << 4);
+}
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void linear_kernel(
     const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, uint16_t* c, int64_t ldc,
@@ -69,82 +85,88 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int64_t m0 = (first_m + in_group % size_m) * kBM;
   const int n0 = (in_group / size_m) * kBN;
 
-  // Copies: wavefront w moves rows 32 w .. 32 w + 31 of each staged tile, 8
-  // rows per 1 KB copy; lane l of copy j carries row 32 w + 8 j + l / 8,
-  // chunk (l % 8) ^ (l / 8) -- its LDS slot is 16 l bytes into the copy, which
-  // is chunk l % 8 of that row after the swizzle.  Rows past M (or N) repeat
-  // the last row: in bounds, and never stored.
-  const int cch = (lane & 7) ^ (lane >> 3);
-  const uint16_t* asrc[kCopies];
-  const uint16_t* bsrc[kCopies];
+  // Copies: the staged A tile is kCopiesA * 4 copies of 1 KB (kRowsPerCopy
+  // rows each), wavefront w taking copies w * kCopiesA + j; the same for B.
+  // Lane l of a copy carries row l / kChunks of it and 16-byte slot
+  // l % kChunks, i.e. source chunk slot ^ key(row) (the copy's first row is a
+  // multiple of kRowsPerCopy, so the key depends on the lane alone).  Rows
+  // past M (or N) repeat the last row: in bounds, and never stored.
+  const int lrow = lane / kChunks;
+  const int cch = (lane % kChunks) ^ swz_key(lrow);
+  const uint16_t* asrc[kCopiesA];
+  const uint16_t* bsrc[kCopiesB];
 #pragma unroll
-  for (int j = 0; j < kCopies; ++j) {
-    const int r = 32 * wave + 8 * j + (lane >> 3);
+  for (int j = 0; j < kCopiesA; ++j) {
+    const int r = (wave * kCopiesA + j) * kRowsPerCopy + lrow;
     const int64_t ra = m0 + r < M ? m0 + r : M - 1;
-    const int rb = n0 + r < N ? n0 + r : N - 1;
     asrc[j] = a + ra * lda + 8 * cch;
+  }
+#pragma unroll
+  for (int j = 0; j < kCopiesB; ++j) {
+    const int r = (wave * kCopiesB + j) * kRowsPerCopy + lrow;
+    const int rb = n0 + r < N ? n0 + r : N - 1;
     bsrc[j] = b + (int64_t)rb * ldb + 8 * cch;
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   auto fetch = [&](int step, int buf) {
     const int k0 = step * kBK;
-    const uint32_t st = lds0 + buf * kStageBytes + wave * (kCopies * 1024);
+    const uint32_t st = lds0 + buf * kStageBytes;
 #pragma unroll
-    for (int j = 0; j < kCopies; ++j) lds_dma16(asrc[j] + k0, uni((int)(st + 1024 * j)));
+    for (int j = 0; j < kCopiesA; ++j)
+      lds_dma16(asrc[j] + k0, uni((int)(st + 1024 * (wave * kCopiesA + j))));
 #pragma unroll
-    for (int j = 0; j < kCopies; ++j)
-      lds_dma16(bsrc[j] + k0, uni((int)(st + kTileBytes + 1024 * j)));
+    for (int j = 0; j < kCopiesB; ++j)
+      lds_dma16(bsrc[j] + k0, uni((int)(st + kTileA + 1024 * (wave * kCopiesB + j))));
   };
 
-  // this wavefront's quarter: rows wm .. wm + 63, columns wn .. wn + 63
-  const int wm = 64 * (wave >> 1), wn = 64 * (wave & 1);
+  // this wavefront's quarter: rows wm .. wm + 16 kXB - 1, columns wn .. wn + 16 kYB - 1
+  const int wm = 16 * kXB * (wave >> 1), wn = 16 * kYB * (wave & 1);
   const int col = lane & 15, grp = lane >> 4;
-  f32x4 acc[4][4];
+  f32x4 acc[kXB][kYB];
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int x = 0; x < kXB; ++x)
 #pragma unroll
-    for (int y = 0; y < 4; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int y = 0; y < kYB; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int steps = K / kBK;
   if (steps > 0) fetch(0, 0);
   for (int t = 0; t < steps; ++t) {
     if (t + 1 < steps) {
       fetch(t + 1, (t + 1) & 1);
-      wait_vmcnt<2 * kCopies>();  // this wavefront's copies of step t have landed
+      wait_vmcnt<kCopiesA + kCopiesB>();  // this wavefront's copies of step t have landed
     } else {
       wait_vmcnt<0>();
     }
     lds_barrier();  // every wavefront's copies of step t have landed
-    const uint16_t* TA = lds + (t & 1) * (kStageBytes / 2);
-    const uint16_t* TB = TA + kTileBytes / 2;
+    const char* TA = reinterpret_cast<const char*>(lds) + (t & 1) * kStageBytes;
+    const char* TB = TA + kTileA;
 #pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
+    for (int kc = 0; kc < kBK / 32; ++kc) {
       // operand of lane (col, grp): row col of the block, k = 32 kc + 8 grp .. + 7
-      u16x8 af[4], bf[4];
+      u16x8 af[kXB], bf[kYB];
 #pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        af[x] = *reinterpret_cast<const u16x8*>(
-            reinterpret_cast<const char*>(TA) + swz(wm + 16 * x + col, 4 * kc + grp));
-        bf[x] = *reinterpret_cast<const u16x8*>(
-            reinterpret_cast<const char*>(TB) + swz(wn + 16 * x + col, 4 * kc + grp));
-      }
+      for (int x = 0; x < kXB; ++x)
+        af[x] = *reinterpret_cast<const u16x8*>(TA + swz(wm + 16 * x + col, 4 * kc + grp));
 #pragma unroll
-      for (int x = 0; x < 4; ++x)
+      for (int y = 0; y < kYB; ++y)
+        bf[y] = *reinterpret_cast<const u16x8*>(TB + swz(wn + 16 * y + col, 4 * kc + grp));
 #pragma unroll
-        for (int y = 0; y < 4; ++y) acc[x][y] = mfma(af[x], bf[y], acc[x][y]);
+      for (int x = 0; x < kXB; ++x)
+#pragma unroll
+        for (int y = 0; y < kYB; ++y) acc[x][y] = mfma(af[x], bf[y], acc[x][y]);
     }
     lds_barrier();  // every wavefront is done with stage t & 1 before it is refilled
   }
 
   // accumulator cell i of block (x, y) in lane (col, grp): row 16 x + 4 grp + i, column 16 y + col
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int x = 0; x < kXB; ++x)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t row = m0 + wm + 16 * x + 4 * grp + i;
       if (row >= M) continue;
 #pragma unroll
-      for (int y = 0; y < 4; ++y) {
+      for (int y = 0; y < kYB; ++y) {
         const int cn = n0 + wn + 16 * y + col;
         if (cn < N) c[row * ldc + cn] = bf16_rne(acc[x][y][i]);
       }

@@ -103,10 +103,10 @@ def test_linear_edges():
     # M = 0: nothing to do
     e = V.linear(torch.zeros((0, 64), dtype=torch.bfloat16, device="cuda"), S.bf16_tensor(b, "cuda"))
     assert e.shape == (0, 20)
-    # K not a multiple of 64: rejected (a missing configuration)
+    # K not a multiple of the K step: rejected (a missing configuration)
     with pytest.raises(V.VdError):
-        V.linear(torch.zeros((3, 96), dtype=torch.bfloat16, device="cuda"),
-                 torch.zeros((20, 96), dtype=torch.bfloat16, device="cuda"))
+        V.linear(torch.zeros((3, 80), dtype=torch.bfloat16, device="cuda"),
+                 torch.zeros((20, 80), dtype=torch.bfloat16, device="cuda"))
     # a row stride that breaks 16-byte alignment: rejected
     big = torch.zeros((3, 68), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(V.VdError):
