@@ -118,13 +118,22 @@ typedef struct {
    * writes new tokens to their private slots before attention reads them, Section 4.1:
    * append + attend in one call).  Rows of a skipped request, or whose page id is outside
    * [0, num_pages), are not written.  Two requests of one call must not hold the same slot
-   * for their query rows. */
+   * for their query rows, and no request of the call may read another request's query-row
+   * slot as a key (the slots of new tokens are private, Section 4.1). */
   const void* k_new;
   const void* v_new;
   /* HOST hint, never value-relevant: nonzero when some pages are read by several requests
-   * of the call (a shared prefix).  K/V are then read with ordinary loads that keep them in
-   * the caches; zero streams them past the caches with non-temporal loads, the faster
-   * choice when each page is read once. */
+   * of the call (a shared prefix, Section 4.1's prefix cache).  It turns on the shared-prefix
+   * pass: the plan launch compares the page tables of adjacent requests and finds groups of
+   * requests whose tables start with the same pages (requests r - 1 and r share 512-key
+   * split k when their entries of splits 0 .. k are equal; a group shares the splits all its
+   * neighbours share, at most 32).  Each shared split is then read once for the query rows
+   * of every member (a request of the group with s_r * (Hq / Hkv) <= 32 whose rows all lie
+   * past the shared splits), with the same operations per row as the request's own split
+   * item, so the output bits do not change; the rest of each request's splits are read by
+   * its own split items.  Not with a sliding window, nor for more than 1024 requests.
+   * Zero: every split is read by its request's items, K/V streamed past the caches with
+   * non-temporal loads (the faster choice when each page is read once). */
   int32_t shared_pages;
   /* Optional output (NULL: not written): [T, Hq] fp32, row t's log-sum-exp in natural log,
    * ln sum_j exp(scale * q.k_j) over the keys the row sees.  The tile update of Appendix A.2
@@ -135,7 +144,8 @@ typedef struct {
 } vd_attn_batch;
 
 /* Bytes of workspace one call needs for the given host-side sizes: the plan
- * (three int32 arrays of num_seqs + 1 and the split work list) and, for every
+ * (int32 arrays of about 3 num_seqs, the shared-prefix list and the split work
+ * list) and, for every
  * (request, KV head, query-head row < 32, 512-key split < ceil(max_context_len /
  * 512)), a partial state of head_dim + 2 floats. */
 int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
@@ -153,18 +163,21 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, voi
 /* The four phases vd_attn_forward runs, in this order, for callers that time
  * or schedule them separately (same batch, same output, same stream, same
  * workspace; their composition is bit-identical to vd_attn_forward):
- *   plan:   only for calls with prefill rows (some s_r * (Hq / Hkv) > 32, by
- *           the hint max_q_len) or more than 256 requests; otherwise it
- *           launches nothing.  Writes k_new / v_new into the pool and, reading
- *           the per-request lengths on the device, the compact work lists of
- *           the split and chunk phases into the workspace (no device-to-host
- *           synchronisation);
+ *   plan:   only for calls with more than 256 requests, with k_new / v_new
+ *           that the split items do not write (some s_r * (Hq / Hkv) > 32 or
+ *           s_r > 16, by the hints), or with the shared_pages hint; otherwise
+ *           it launches nothing.  Writes k_new / v_new into the pool and,
+ *           reading the per-request lengths and page tables on the device, the
+ *           work lists of the split and shared-prefix phases into the
+ *           workspace (no device-to-host synchronisation);
  *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
- *           per (request, KV head, 512-key split).  Without a plan launch,
- *           every workgroup derives its item from the lengths and the items
- *           write the call's new tokens themselves.  A request with one split
- *           writes its output rows directly; otherwise each item writes a
- *           partial state;
+ *           per (request, KV head, 512-key split, 16 query-head rows), after
+ *           the shared-prefix items (shared_pages hint) -- one per (group, KV
+ *           head, 128 query-head rows of its members, shared split).  Without
+ *           a plan launch, every workgroup derives its items from the lengths
+ *           and the items write the call's new tokens themselves.  A request
+ *           with one split writes its output rows directly; otherwise each
+ *           item writes a partial state;
  *   chunks: rows of requests with s_r * (Hq / Hkv) > 32 -- one work item per
  *           (request, KV head, 128 query-head rows); folds the splits in
  *           registers and writes their output rows;
@@ -180,12 +193,14 @@ int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* batch, void* o
 int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* batch, void* out,
                           const void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* The splits and chunks phases with their kernel timed: identical launches
+/* The splits and chunks phases with their kernels timed: identical launches
  * and results, and in addition `start` and `stop` (hipEvent_t the caller
- * created with timing enabled, or NULL) are recorded by the kernel's own
- * dispatch (hipExtLaunchKernel) at its start and end, with no separate marker
- * packet in the stream.  When the phase launches no kernel (no such rows),
- * both events are recorded back to back on `stream`. */
+ * created with timing enabled, or NULL) are recorded by the kernel dispatches
+ * themselves (hipExtLaunchKernel): `start` at the start of the phase's first
+ * kernel (the shared-prefix kernel when it runs), `stop` at the end of its
+ * last, with no separate marker packet in the stream.  When the phase
+ * launches no kernel (no such rows), both events are recorded back to back
+ * on `stream`. */
 int vd_attn_forward_splits_timed(const vd_attn* h, const vd_attn_batch* batch, void* out,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop);

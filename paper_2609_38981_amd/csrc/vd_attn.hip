@@ -68,6 +68,14 @@ struct Params {
   // the split workgroups derive their items from the lengths (no plan launch)
   int inwave;
   float* lse;  // optional [T, Hq] log-sum-exp output
+  // shared-prefix pass (calls with the shared_pages hint): the plan launch
+  // finds groups of adjacent requests whose page tables start with the same
+  // pages; the shared-prefix kernel computes their leading splits once
+  int casc;
+  int32_t* casc_hdr;  // {listed groups, items per KV head}
+  int32_t* casc_seq;  // [num_seqs] leading splits of the request computed by it (0: none)
+  int32_t* casc_off;  // [listed groups + 1] first item of each group
+  int4* casc_grp;     // [listed groups] {first member, last member + 1, splits, first token}
 };
 
 struct Req {
@@ -310,19 +318,228 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-// Work-list entry of one split item: request, KV head, split index and the
-// request's lengths, so that a split wavefront reaches its first K/V loads
-// after a single scalar load.  r = -1 marks an unused grid slot.
-constexpr int kItemInts = 8;  // {r, g, k, n, q0, s, 0, 0}
+// A split item covers 16 query-head rows ("columns") of its request: a
+// request with more (s * G in 17 .. 32) has an item per split and column half.
+__device__ __forceinline__ int column_halves(const Req& R, int G) { return R.s * G > 16 ? 2 : 1; }
+
+// Length of the split work list: an upper bound of the split items.
+__host__ __device__ __forceinline__ int64_t split_slots(const Params& P) {
+  return (int64_t)P.num_seqs * P.hkv * P.max_splits * (P.split_cols / 16);
+}
+
+// Work-list entry of one split item: request, KV head, split index, the
+// request's lengths and the column half, so that a split wavefront reaches
+// its first K/V loads after a single scalar load.  r = -1 marks an unused slot.
+constexpr int kItemInts = 8;  // {r, g, k, n, q0, s, half, 0}
 // Number of counters of the planning scan: whole splits, chunk q-tiles, and
 // the last (partial) splits by their tile count, 8 down to 1.
 constexpr int kPlanCounters = 2 + kTilesPerSplit;
 
 __device__ __forceinline__ void put_item(const Params& P, int64_t idx, int r, int g, int k,
-                                         const Req& R) {
+                                         const Req& R, int half) {
   int4* e = reinterpret_cast<int4*>(P.items + idx * kItemInts);
   e[0] = int4{r, g, k, R.n};
-  e[1] = int4{R.q0, R.s, 0, 0};
+  e[1] = int4{R.q0, R.s, half, 0};
+}
+
+// ---------------------------------------------------------------------------
+// shared-prefix planning (plan workgroup 0, calls with the shared_pages hint)
+// ---------------------------------------------------------------------------
+// Requests of a call the shared-prefix pass examines, and the leading splits
+// of a request it may cover.
+constexpr int kCascMaxSeqs = 1024;
+constexpr int kCascMaxSplits = 32;
+constexpr int kPagesPerSplit = kSplitKeys / kPage;
+
+// Inclusive prefix sum over the 1024 threads of the workgroup; *total gets
+// the sum over all of them.  Every thread of the workgroup must call it.
+__device__ __forceinline__ int block_incl_scan(int v, int* total) {
+  __shared__ int wtot[16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int x = wave_incl_scan(v);
+  if (lane == 63) wtot[wave] = x;
+  __syncthreads();
+  int pre = 0, all = 0;
+  for (int w = 0; w < 16; ++w) {
+    const int t = wtot[w];
+    pre += w < wave ? t : 0;
+    all += t;
+  }
+  __syncthreads();  // wtot is reused by the next call
+  *total = all;
+  return x + pre;
+}
+
+// Reduction over the lanes from this one to the end of its run of equal
+// keys, for keys that do not decrease across the lanes (a run is contiguous):
+// the first lane of each run gets the run's min (MIN) or sum.
+template <bool MIN>
+__device__ __forceinline__ int run_reduce(int v, int key) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_down(v, o, 64), tk = __shfl_down(key, o, 64);
+    if (lane + o < 64 && tk == key) v = MIN ? min(v, t) : v + t;
+  }
+  return v;
+}
+
+__device__ __forceinline__ bool run_start(int key) {
+  const int lane = __lane_id();
+  const int prev = __shfl_up(key, 1, 64);
+  return lane == 0 || prev != key;
+}
+
+// Groups of adjacent requests that share leading splits, listed for the
+// shared-prefix kernel.
+//  * Requests r - 1 and r (both valid) share split k when their page-table
+//    entries of splits 0 .. k are equal: the same physical pages, hence the
+//    same keys and values.  sh(r) counts the leading splits they share (at
+//    most kCascMaxSplits, within both contexts).
+//  * A group is a maximal run of requests with sh >= 1 between neighbours; it
+//    shares c = the smallest sh of the run.  An invalid request is a group of
+//    its own, so the query rows of a group's requests are consecutive.
+//  * A member is a request of a group on the split path whose query rows all
+//    lie past the c shared splits (n - s >= 512 c): each of its rows sees
+//    every key of them, and none of them is a new token of the call.
+//  * A group with at least two members is listed: its members' splits
+//    0 .. c - 1 are computed by the shared-prefix kernel (csq[r] = c), their
+//    later splits by the split kernel.  Its items are (tile of 128 query-head
+//    rows over the members' query rows, shared split).
+// Requires num_seqs <= kCascMaxSeqs and 1024 threads.  One round trip to
+// memory: the lengths and every page-table entry compared are loaded
+// together (the comparison runs over the first E entries of every row,
+// E = 32 * min(kCascMaxSplits, max_context_len / 512) within the table stride,
+// and is cut to the pair's own contexts afterwards).
+template <int W>  // entries per load: 1, or 4 for a 16-byte aligned table
+__device__ __forceinline__ void compare_rows(const Params& P, int B, int E, int* fd) {
+  typedef int vec __attribute__((ext_vector_type(W)));
+  const int U = E / W;                        // loads per row
+  const int flat = (B - 1) * U;               // pairs (r - 1, r), r = 1 .. B - 1
+  constexpr int J = 32 / W < 16 ? 32 / W : 16;  // loads of each row per thread and round
+  for (int f0 = 0; f0 < flat; f0 += 1024 * J) {
+    vec a[J], b[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int f = f0 + (int)threadIdx.x + 1024 * j;
+      const bool ok = f < flat;
+      const int r = 1 + (ok ? f / U : 0), u = ok ? f % U : 0;
+      const vec* row = reinterpret_cast<const vec*>(P.pt + (int64_t)r * P.pt_stride) + u;
+      a[j] = ok ? row[0] : vec{};
+      b[j] = ok ? *reinterpret_cast<const vec*>(P.pt + (int64_t)(r - 1) * P.pt_stride + u * W) : vec{};
+    }
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int f = f0 + (int)threadIdx.x + 1024 * j;
+      if (f < flat) {
+        int e = E;  // first differing entry of the unit
+#pragma unroll
+        for (int w = W - 1; w >= 0; --w)
+          if (a[j][w] != b[j][w]) e = (f % U) * W + w;
+        if (e < E) atomicMin(&fd[1 + f / U], e);
+      }
+    }
+  }
+}
+
+__device__ void plan_prefix(const Params& P, int* csq) {
+  __shared__ int fd[kCascMaxSeqs];   // first entry where rows r - 1 and r differ
+  __shared__ int sq[kCascMaxSeqs + 1], sn[kCascMaxSeqs];  // cu and n
+  __shared__ int gmin[kCascMaxSeqs], gcnt[kCascMaxSeqs], gfirst[kCascMaxSeqs],
+      glast[kCascMaxSeqs];
+  const int tid = threadIdx.x;
+  const int B = P.num_seqs;
+  const int r = tid;
+  const int E = kPagesPerSplit * min(kCascMaxSplits, min(P.max_ctx / kSplitKeys,
+                                                          P.pt_stride / kPagesPerSplit));
+  fd[tid] = E;
+  __syncthreads();
+  int q0 = 0, q1 = 0, n = 0;
+  if (r < B) {
+    q0 = P.cu[r];
+    q1 = P.cu[r + 1];
+    n = P.ctx[r];
+  }
+  if (E > 0) {
+    if ((reinterpret_cast<uintptr_t>(P.pt) % 16 == 0) && P.pt_stride % 4 == 0)
+      compare_rows<4>(P, B, E, fd);
+    else
+      compare_rows<1>(P, B, E, fd);
+  }
+  if (r < B) {
+    sq[r] = q0;
+    sn[r] = n;
+    if (r == B - 1) sq[B] = q1;
+  }
+  __syncthreads();
+  // Requests r - 1 and r (both valid) share split k when their entries of
+  // splits 0 .. k are equal and both contexts reach past split k.
+  int sh = 0, vis = -1;
+  if (r < B) {
+    const Req R = make_req(P, q0, q1, n);
+    if (R.valid && R.s * P.G <= P.split_cols) vis = (R.n - R.s) / kSplitKeys;
+    if (r > 0 && R.valid && make_req(P, sq[r - 1], q0, sn[r - 1]).valid)
+      sh = min(fd[r] / kPagesPerSplit, min(R.n, sn[r - 1]) / kSplitKeys);
+  }
+  const bool head = r < B && (r == 0 || sh == 0);
+  int ngroups;
+  const int gid = block_incl_scan(head ? 1 : 0, &ngroups) - 1;  // group of r (r < B)
+  if (head) {
+    gmin[gid] = kCascMaxSplits + 1;  // a group of one request shares nothing
+    gcnt[gid] = 0;
+    gfirst[gid] = kCascMaxSeqs;
+    glast[gid] = -1;
+  }
+  __syncthreads();
+  // per-group statistics: a wavefront's lanes are consecutive requests, so
+  // each run of one group in it adds one atomic
+  const int key = r < B ? gid : kCascMaxSeqs;  // gid does not decrease with r
+  {
+    const int v = run_reduce<true>(r < B && !head ? sh : kCascMaxSplits + 1, key);
+    if (r < B && run_start(key)) atomicMin(&gmin[gid], v);
+  }
+  __syncthreads();
+  const int c = r < B ? gmin[gid] : 0;
+  const bool member = r < B && c <= kCascMaxSplits && vis >= c;
+  {
+    const int cnt = run_reduce<false>(member ? 1 : 0, key);
+    const int lo = run_reduce<true>(member ? r : kCascMaxSeqs, key);
+    const int hi = -run_reduce<true>(member ? -r : 1, key);
+    if (r < B && run_start(key) && cnt > 0) {
+      atomicAdd(&gcnt[gid], cnt);
+      atomicMin(&gfirst[gid], lo);
+      atomicMax(&glast[gid], hi);
+    }
+  }
+  __syncthreads();
+  const int take = member && gcnt[gid] >= 2 ? c : 0;
+  if (r < B) {
+    csq[r] = take;
+    P.casc_seq[r] = take;
+  }
+  // the list: groups with at least two members, in request order, each with
+  // an item per (tile of 128 query-head rows over the members' query rows,
+  // shared split)
+  const int gi = tid;
+  const bool listed = gi < ngroups && gcnt[gi] >= 2;
+  int items = 0;
+  if (listed)
+    items = gmin[gi] *
+            (int)(((int64_t)(sq[glast[gi] + 1] - sq[gfirst[gi]]) * P.G + kChunkCols - 1) /
+                  kChunkCols);
+  int nlisted, nitems;
+  const int li = block_incl_scan(listed ? 1 : 0, &nlisted) - 1;
+  const int ioff = block_incl_scan(items, &nitems) - items;
+  if (listed) {
+    P.casc_grp[li] = int4{gfirst[gi], glast[gi] + 1, gmin[gi], sq[gfirst[gi]]};
+    P.casc_off[li] = ioff;
+  }
+  if (tid == 0) {
+    P.casc_off[nlisted] = nitems;
+    P.casc_hdr[0] = nlisted;
+    P.casc_hdr[1] = nitems;
+  }
+  __syncthreads();
 }
 
 template <int D>
@@ -332,6 +549,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
     append_rows<D>(P, (int64_t)(blockIdx.x - 1) * 16 + (threadIdx.x >> 6));
     return;
   }
+  __shared__ int csq[kCascMaxSeqs];  // leading splits of request r the shared-prefix kernel runs
+  if (P.casc) plan_prefix(P, csq);
   if (P.inwave) return;  // the split and chunk workgroups plan for themselves
   constexpr int NC = kPlanCounters;
   __shared__ int wsum[NC][16];  // per-wavefront totals of each counter
@@ -349,17 +568,20 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
   // last split has t tiles (Hkv items each), counted with ballots.
   for (int r0 = 0; r0 < P.num_seqs; r0 += 1024) {
     const int r = r0 + tid;
-    int cfull = 0, cchunk = 0, cls = -1;
+    int cfull = 0, cchunk = 0, cls = -1, h = 1;
     if (r < P.num_seqs) {
       const Req R = load_req(P, r);
       if (R.valid) {
         const int ncols = R.s * P.G;
         if (ncols <= P.split_cols) {
+          h = column_halves(R, P.G);
           // splits before the one holding the first row's window start
           // hold no visible key and get no item
           const int lo_min = window_lo(R.n - R.s, P.window);
-          const int kfirst = lo_min / kSplitKeys, nfull = R.n / kSplitKeys;
-          cfull = P.hkv * max(0, nfull - kfirst);
+          // (and before those of the shared-prefix kernel)
+          const int kfirst = max(lo_min / kSplitKeys, P.casc ? csq[r] : 0);
+          const int nfull = R.n / kSplitKeys;
+          cfull = P.hkv * h * max(0, nfull - kfirst);
           if (R.n % kSplitKeys) {
             // tiles the last split's items run
             const int t = (R.n + kTileKeys - 1) / kTileKeys -
@@ -372,12 +594,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
       }
     }
     const int ifull = wave_incl_scan(cfull), ichunk = wave_incl_scan(cchunk);
-    int rank = 0;  // requests of the same class below this lane in the wavefront
+    int rank = 0;  // items per KV head of the same class below this lane in the wavefront
 #pragma unroll
     for (int c = 2; c < NC; ++c) {
-      const unsigned long long m = __ballot(cls == c);
-      rank = cls == c ? __popcll(m & below) : rank;
-      if (lane == 0) wsum[c][wave] = __popcll(m) * P.hkv;
+      const unsigned long long m = __ballot(cls == c), m2 = __ballot(cls == c && h == 2);
+      rank = cls == c ? __popcll(m & below) + __popcll(m2 & below) : rank;
+      if (lane == 0) wsum[c][wave] = (__popcll(m) + __popcll(m2)) * P.hkv;
     }
     if (lane == 63) {
       wsum[0][wave] = ifull;
@@ -448,16 +670,18 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
       R.valid = true;
       const int rfo = __builtin_amdgcn_readlane(fo, j), rpo = __builtin_amdgcn_readlane(po, j);
       const int nfull = R.n / kSplitKeys;
-      const int kfirst = window_lo(R.n - R.s, P.window) / kSplitKeys;
-      const int nf = nfull - kfirst;  // whole splits with an item
-      for (int idx = lane; idx < P.hkv * nf; idx += 64)
-        put_item(P, (int64_t)rfo + idx, r, idx / nf, kfirst + idx % nf, R);
+      const int kfirst = max(window_lo(R.n - R.s, P.window) / kSplitKeys, P.casc ? csq[r] : 0);
+      const int nf = nfull - kfirst;  // whole splits with items
+      const int h = column_halves(R, P.G);
+      // items (KV head, split, half), halves adjacent
+      for (int idx = lane; idx < P.hkv * nf * h; idx += 64)
+        put_item(P, (int64_t)rfo + idx, r, idx / (nf * h), kfirst + idx % (nf * h) / h, R, idx % h);
       if (R.n % kSplitKeys)
-        for (int g = lane; g < P.hkv; g += 64) put_item(P, (int64_t)rpo + g, r, g, nfull, R);
+        for (int x = lane; x < P.hkv * h; x += 64) put_item(P, (int64_t)rpo + x, r, x / h, nfull, R, x % h);
     }
   }
-  // Pass 3: grid slots past the list exit at once
-  const int64_t upper = (int64_t)P.num_seqs * P.hkv * P.max_splits;
+  // Pass 3: slots past the list end the split workgroups' loops
+  const int64_t upper = split_slots(P);
   for (int64_t i = total + tid; i < upper; i += 1024) P.items[i * kItemInts] = -1;
 }
 
@@ -593,11 +817,13 @@ __device__ __forceinline__ void stage_v_new(const Params& P, uint16_t* lds, int 
   }
 }
 
+// Substitutes the new V rows into the tile's operands; with `store` also
+// writes them to their pool slots.
 template <int D>
 __device__ __forceinline__ void apply_v_new(const Params& P, const uint16_t* lds,
                                             const int64_t (&pb)[kPagesPerTile],
                                             u16x4 (&vh)[D / 16][kPagesPerTile], int j0,
-                                            const Req& R) {
+                                            const Req& R, bool store) {
   const int lane = __lane_id(), col = lane & 15, grp = lane >> 4;
   wait_vmcnt<0>();  // the staged rows (and every load of the tile) have landed
 #pragma unroll
@@ -618,7 +844,7 @@ __device__ __forceinline__ void apply_v_new(const Params& P, const uint16_t* lds
       int64_t blk = -1;
 #pragma unroll
       for (int b = 0; b < kPagesPerTile; ++b) blk = bv == b ? pb[b] : blk;
-      if (blk >= 0) {
+      if (store && blk >= 0) {
         uint16_t* dst = const_cast<uint16_t*>(P.vpool) + blk * (kPage * D) + 4 * lane + i;
 #pragma unroll
         for (int m = 0; m < D / 16; ++m) dst[256 * m] = t[m];
@@ -628,11 +854,12 @@ __device__ __forceinline__ void apply_v_new(const Params& P, const uint16_t* lds
 }
 
 // One split item: the tiles of split k of request r, KV head g, for NA
-// column blocks of 16 query-head rows.  WIN: the handle has a sliding window.
-// vlds: LDS rows for the call's new V rows (kMaxNewRows * D bf16).
+// column blocks of 16 query-head rows, from column 16 * NA * half.  WIN: the
+// handle has a sliding window.  vlds: LDS rows for the call's new V rows
+// (kMaxNewRows * D bf16); the item of half 0 writes them to the pool.
 template <int D, int NA, bool WIN, bool NT>
 __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k, const Req& R,
-                                           uint16_t* vlds) {
+                                           uint16_t* vlds, int half) {
   const int window = WIN ? P.window : 0;
   const int lane = __lane_id();
   const int col = lane & 15, grp = lane >> 4;
@@ -642,9 +869,10 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
   int pos[NA], lo[NA];  // visible keys of the column: lo .. pos
   u16x8 qf[NA][D / 32];
   State<D> st[NA];
+  const int cbase = 16 * NA * half;
 #pragma unroll
   for (int nb = 0; nb < NA; ++nb) {
-    const int c = nb * 16 + col;
+    const int c = cbase + nb * 16 + col;
     const bool v = c < ncols;
     pos[nb] = v ? R.n - R.s + c / P.G : -1;
     lo[nb] = window_lo(pos[nb], window);
@@ -685,11 +913,11 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 #pragma unroll
     for (int b = 0; b < kPagesPerTile; ++b)
       pb[b] = page_block(P, ptrow, (kt + 1) * kPagesPerTile + b, R.n, g);
-    if (newtile) store_k_new<D>(P, pb_cur, kf, j0, R);
+    if (newtile && half == 0) store_k_new<D>(P, pb_cur, kf, j0, R);
     if (!full) mask_k<D>(pb_cur, j0, R.n, kf);
     f32x4 acc[NA][kPagesPerTile];
     tile_scores<D, NA>([&](int b, int ks) { return kf[b][ks]; }, qf, acc);
-    if (newtile) apply_v_new<D>(P, vlds, pb_cur, vh, j0, R);
+    if (newtile) apply_v_new<D>(P, vlds, pb_cur, vh, j0, R, half == 0);
     if (!full) mask_v<D>(pb_cur, j0, R.n, vh);
     TileWeights w[NA];
     bool open = true;  // every key of the tile visible to every column
@@ -720,7 +948,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 #pragma unroll
     for (int nb = 0; nb < NA; ++nb) {
       if (pos[nb] < 0) continue;
-      const int c = nb * 16 + col;
+      const int c = cbase + nb * 16 + col;
       store_row<D>(P, st[nb].u, st[nb].m, st[nb].z, R.q0 + c / P.G, g * P.G + c % P.G);
     }
     return;
@@ -728,7 +956,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
   // partial state of split k for every column that has a visible key in it
 #pragma unroll
   for (int nb = 0; nb < NA; ++nb) {
-    const int c = nb * 16 + col;
+    const int c = cbase + nb * 16 + col;
     if (pos[nb] < 0 || k > pos[nb] / kSplitKeys || k < lo[nb] / kSplitKeys) continue;
     const int64_t pidx = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS + k;
     if (grp == 0) {
@@ -754,8 +982,9 @@ constexpr int kInWaveChunks = 4;
 constexpr int kInWaveMaxSeqs = 64 * kInWaveChunks;
 
 struct SplitRef {
-  int r, g, k;
+  int r, g, k, half;
   Req R;
+  int per_xcd;  // items each XCD takes (slots b with b / 8 < per_xcd hold one)
 };
 
 // Inclusive prefix sum over the 64 lanes with DPP moves: shifts by 1, 2, 4
@@ -771,28 +1000,31 @@ __device__ __forceinline__ int wave_scan_dpp(int v) {
   return v;
 }
 
-__device__ __forceinline__ bool inwave_split_item(const Params& P, SplitRef& out) {
+__device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, SplitRef& out) {
   constexpr int C = kInWaveChunks;
   const int lane = __lane_id();
   const unsigned long long below = (1ull << lane) - 1;
   // every load first (indices clamped into [0, num_seqs)), then the arithmetic
-  int cq0[C], cq1[C], cn[C];
+  int cq0[C], cq1[C], cn[C], ccs[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     const int rr = min(64 * c + lane, P.num_seqs - 1);
     cq0[c] = P.cu[rr];
     cq1[c] = P.cu[rr + 1];
     cn[c] = P.ctx[rr];
+    ccs[c] = P.casc ? P.casc_seq[rr] : 0;  // leading splits run by the shared-prefix kernel
   }
-  // per request: whole-split items nf from split kfst, and the tile count cls
-  // of its last partial split (0: none)
-  int nf[C], kfst[C], cls[C], incl[C];
+  // per request: whole splits nf from split kfst, the tile count cls of its
+  // last partial split (0: none), and its column halves h (an item per split
+  // and half: whole-split items nf * h)
+  int nf[C], kfst[C], cls[C], hv[C], incl[C];
   int whole = 0;
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     nf[c] = 0;
     kfst[c] = 0;
     cls[c] = 0;
+    hv[c] = 1;
     incl[c] = 0;
     if (64 * c >= P.num_seqs) continue;  // wave-uniform: no request in this chunk
     if (64 * c + lane < P.num_seqs) {
@@ -800,41 +1032,47 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, SplitRef& out
       if (R.valid && R.s * P.G <= P.split_cols) {
         const int lo_min = window_lo(R.n - R.s, P.window);
         const int nfull = R.n / kSplitKeys;
-        kfst[c] = lo_min / kSplitKeys;
+        kfst[c] = max(lo_min / kSplitKeys, ccs[c]);
         nf[c] = max(0, nfull - kfst[c]);
+        hv[c] = column_halves(R, P.G);
         if (R.n % kSplitKeys)
           cls[c] = (R.n + kTileKeys - 1) / kTileKeys -
                    max(nfull * kTilesPerSplit, lo_min / kTileKeys);
       }
     }
-    incl[c] = wave_scan_dpp(nf[c]);
+    incl[c] = wave_scan_dpp(nf[c] * hv[c]);
     whole += __builtin_amdgcn_readlane(incl[c], 63);
   }
   int partial = 0;
 #pragma unroll
-  for (int c = 0; c < C; ++c) partial += __popcll(__ballot(cls[c] > 0));
+  for (int c = 0; c < C; ++c)
+    partial += __popcll(__ballot(cls[c] > 0)) + __popcll(__ballot(cls[c] > 0 && hv[c] == 2));
   const int per_head = whole + partial;
   const int total = per_head * P.hkv;
   const int per_xcd = (total + 7) / 8;
-  const int jx = (int)(blockIdx.x / 8);
+  out.per_xcd = per_xcd;
+  const int jx = vb / 8;
   if (jx >= per_xcd) return false;
-  const int i = (int)(blockIdx.x % 8) * per_xcd + jx;
+  const int i = (vb % 8) * per_xcd + jx;
   if (i >= total) return false;
   out.g = uni(i / per_head);
   int idx = i - out.g * per_head;
   const bool is_whole = idx < whole;
-  int j = -1, cj = 0, kj = 0;
+  int j = -1, cj = 0, kj = 0, hj = 0;
   if (is_whole) {
     int base = 0;
 #pragma unroll
     for (int c = 0; c < C; ++c) {
       const int tot = __builtin_amdgcn_readlane(incl[c], 63);
       if (j < 0 && idx < base + tot) {
-        // the first request whose inclusive item count passes idx
+        // the first request whose inclusive item count passes idx; its items
+        // are (split, half), halves adjacent
         j = __builtin_ctzll(__ballot(incl[c] > idx - base));
         cj = c;
-        kj = __builtin_amdgcn_readlane(kfst[c], j) + idx - base -
-             __builtin_amdgcn_readlane(incl[c] - nf[c], j);
+        const int h = __builtin_amdgcn_readlane(hv[c], j);
+        const int local = idx - base - __builtin_amdgcn_readlane(incl[c] - nf[c] * hv[c], j);
+        kj = __builtin_amdgcn_readlane(kfst[c], j) + local / h;
+        hj = local % h;
       }
       base += tot;
     }
@@ -845,12 +1083,15 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, SplitRef& out
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         const unsigned long long m = __ballot(cls[c] == t);
-        const int cnt = __popcll(m);
+        const unsigned long long m2 = __ballot(cls[c] == t && hv[c] == 2);
+        const int cnt = __popcll(m) + __popcll(m2);
         if (j < 0) {
           if (idx < cnt) {
-            // the idx-th request (ascending) of this class
-            j = __builtin_ctzll(__ballot(cls[c] == t && __popcll(m & below) == idx));
+            // the item idx of this class: requests ascending, halves adjacent
+            const int before = __popcll(m & below) + __popcll(m2 & below);
+            j = __builtin_ctzll(__ballot(cls[c] == t && before <= idx && idx < before + hv[c]));
             cj = c;
+            hj = idx - __builtin_amdgcn_readlane(before, j);
           } else {
             idx -= cnt;
           }
@@ -858,23 +1099,26 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, SplitRef& out
       }
   }
   if (j < 0) return false;
-  int q0 = 0, q1 = 0, n = 0;
+  int q0 = 0, q1 = 0, n = 0, cc = 0;
 #pragma unroll
   for (int c = 0; c < C; ++c)
     if (c == cj) {
       q0 = __builtin_amdgcn_readlane(cq0[c], j);
       q1 = __builtin_amdgcn_readlane(cq1[c], j);
       n = __builtin_amdgcn_readlane(cn[c], j);
+      cc = __builtin_amdgcn_readlane(ccs[c], j);
     }
   out.r = uni(64 * cj + j);
   out.R = make_req(P, q0, q1, n);
   // a whole split found above, or the request's last (partial) split
   out.k = uni(is_whole ? kj : n / kSplitKeys);
+  out.half = uni(hj);
   // the item addresses only the request's own table row, rows and partial
-  // states: check that it is one of the request's splits
+  // states: check that it is one of the request's splits and halves
   return out.r < P.num_seqs && out.g < P.hkv && out.R.valid && out.R.s * P.G <= P.split_cols &&
-         out.k >= window_lo(out.R.n - out.R.s, P.window) / kSplitKeys &&
-         out.k <= (out.R.n - 1) / kSplitKeys;
+         out.k >= window_lo(out.R.n - out.R.s, P.window) / kSplitKeys && out.k >= cc &&
+         out.k <= (out.R.n - 1) / kSplitKeys && out.half >= 0 &&
+         out.half < column_halves(out.R, P.G);
 }
 
 // Chunk items without a plan launch (at most kInWaveMaxSeqs requests): the
@@ -944,44 +1188,53 @@ __device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& 
          qt < (ncols + kChunkCols - 1) / kChunkCols;
 }
 
-// One wavefront per workgroup: a finished item frees its slot at once, which
-// keeps the end of the launch short when item durations vary.  NT: K/V are
-// streamed with non-temporal loads.
-template <int D, int NB, bool WIN, bool NT>
+// One wavefront per workgroup, 16 columns per item (two wavefronts per SIMD
+// at head_dim 128): a finished item frees its slot at once, which keeps the
+// end of the launch short when item durations vary.  The grid is capped at
+// about twice the wavefronts the chip holds at once; workgroup b
+// takes the slots b, b + grid, b + 2 grid, ... (the grid is a multiple of the
+// 8 XCDs, so its slots stay on its XCD) until one is past the items.  NT:
+// K/V are streamed with non-temporal loads.
+template <int D, bool WIN, bool NT>
 __global__ __launch_bounds__(64) void split_kernel(Params P) {
-  int r, g, k;
-  Req R;
-  if (P.inwave) {
-    SplitRef it;
-    if (!inwave_split_item(P, it)) return;
-    r = uni(it.r);
-    g = it.g;
-    k = uni(it.k);
-    R = it.R;
-  } else {
-    // the item's work-list entry: all 8 words in one scalar load, so that the
-    // exit test and the item's fields cost a single round trip (the list is
-    // read-only for the whole launch)
-    typedef int int8v __attribute__((ext_vector_type(8)));
-    const int32_t* ep = P.items + (int64_t)blockIdx.x * kItemInts;
-    int8v ev;
-    asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(ev) : "s"(ep) : "memory");
-    const int4 e0 = int4{ev[0], ev[1], ev[2], ev[3]}, e1 = int4{ev[4], ev[5], ev[6], ev[7]};
-    r = e0.x;
-    if (r < 0) return;
-    g = e0.y;
-    k = e0.z;
-    R.n = e0.w;
-    R.q0 = e1.x;
-    R.s = e1.y;
-    R.valid = true;
-  }
   __shared__ __attribute__((aligned(16))) uint16_t vlds[kMaxNewRows * D];
-  // column blocks actually used by this request: one wave-uniform dispatch
-  if (NB == 2 && R.s * P.G > 16)
-    split_item<D, NB, WIN, NT>(P, r, g, k, R, vlds);
-  else
-    split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds);
+  const int64_t slots = split_slots(P);  // work-list length
+  int per_xcd = 0;
+  for (int vb = blockIdx.x;; vb += gridDim.x) {
+    int r, g, k, half;
+    Req R;
+    if (P.inwave) {
+      SplitRef it;
+      if (!inwave_split_item(P, vb, it)) return;
+      per_xcd = it.per_xcd;
+      r = uni(it.r);
+      g = it.g;
+      k = uni(it.k);
+      half = it.half;
+      R = it.R;
+    } else {
+      if (vb >= slots) return;
+      // the slot's work-list entry: all 8 words in one scalar load, so that
+      // the exit test and the item's fields cost a single round trip (the
+      // list is read-only for the whole launch)
+      typedef int int8v __attribute__((ext_vector_type(8)));
+      const int32_t* ep = P.items + (int64_t)vb * kItemInts;
+      int8v ev;
+      asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(ev) : "s"(ep) : "memory");
+      const int4 e0 = int4{ev[0], ev[1], ev[2], ev[3]}, e1 = int4{ev[4], ev[5], ev[6], ev[7]};
+      r = e0.x;
+      if (r < 0) return;  // the list's valid entries come first
+      g = e0.y;
+      k = e0.z;
+      R.n = e0.w;
+      R.q0 = e1.x;
+      R.s = e1.y;
+      half = e1.z;
+      R.valid = true;
+    }
+    split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds, half);
+    if (P.inwave && (vb + (int)gridDim.x) / 8 >= per_xcd) return;  // no further slot holds an item
+  }
 }
 
 // Contexts of up to this many splits are merged by the short merge kernel.
@@ -1359,6 +1612,201 @@ constexpr size_t chunk_lds_bytes() {
 }
 
 // ---------------------------------------------------------------------------
+// shared-prefix kernel: one workgroup (4 wavefronts x 32 columns) per (KV
+// head, listed group, 128 query-head rows of the group's query rows, shared
+// split k).  Split k is read once for all these rows: its K/V tiles stream
+// through the LDS ring as in the chunk kernel (page ids from the first
+// member's table row, which every member shares), and each column runs the
+// same per-tile operations as the split item (request, KV head, k) of its own
+// request would (every key of a shared split is visible to it) and stores the
+// same partial state; the merge folds it with the request's other splits.
+// Rows of requests in the group's range that are not members are padding
+// columns (zero queries, never stored).
+// ---------------------------------------------------------------------------
+// One item i of the list (per_head items per KV head); every value read from
+// the list is checked before it addresses memory.
+template <int D>
+__device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups, int per_head,
+                                            uint16_t* lds, int* scu) {
+  constexpr int NB = 2;
+  constexpr int BLK = kPage * D;
+  constexpr int NBLK = 2 * kPagesPerTile;
+  constexpr int TILE = NBLK * BLK;
+  constexpr int WCH = TILE / (4 * 512);
+  constexpr int STAGES = kChunkStages;
+  const int wave = uni(threadIdx.x >> 6);
+  const int lane = __lane_id();
+  const int col = lane & 15, grp = lane >> 4;
+  const int g = uni(i / per_head);
+  const int rem = i - g * per_head;
+  const int li = find_req(P.casc_off, ngroups, rem);
+  const int4 gr = P.casc_grp[li];
+  const int first = uni(gr.x), end = uni(gr.y), cg = uni(gr.z);
+  if (first < 0 || end > P.num_seqs || end - first < 2 || cg < 1 || cg > kCascMaxSplits ||
+      cg > P.max_splits)
+    return;
+  const int t0 = P.cu[first];
+  const int x = uni(rem - P.casc_off[li]);  // (tile, split) of the group
+  const int c0 = (x / cg) * kChunkCols, k = x % cg;
+  const int ncols = (P.cu[end] - t0) * P.G;
+  if (c0 < 0 || c0 >= ncols) return;
+  // the requests of the item's rows: consecutive, from the one holding its
+  // first row (a group's requests are valid, so cu is increasing over it)
+  const int r0 = first + find_req(P.cu + first, end - first, t0 + c0 / P.G);
+  const int nr = min(end - r0, kChunkCols);  // the rows reach requests r0 .. r0 + nr - 1
+  if ((int)threadIdx.x <= nr) scu[threadIdx.x] = P.cu[r0 + threadIdx.x];
+  __syncthreads();
+
+  bool live[NB];
+  int64_t pidx[NB];  // the column's partial state of split k
+  u16x8 qf[NB][D / 32];
+  State<D> st[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int c = c0 + wave * 32 + nb * 16 + col;
+    bool v = c < ncols;
+    int t = 0, hh = 0;
+    pidx[nb] = 0;
+    if (v) {
+      t = t0 + c / P.G;
+      hh = c % P.G;
+      int lo = 0, hi = nr;  // scu[lo] <= t < scu[hi]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (scu[mid] <= t) lo = mid; else hi = mid;
+      }
+      const int r = r0 + lo;
+      const int cl = (t - scu[lo]) * P.G + hh;  // the column's index among its request's
+      // a member (its rows are on the split path), and the row is its own
+      v = P.casc_seq[r] == cg && t >= scu[lo] && t < scu[lo + 1] && cl < kSplitCols;
+      pidx[nb] = ((int64_t)(r * P.hkv + g) * kSplitCols + cl) * P.max_splits + k;
+    }
+    live[nb] = v;
+    load_q<D>(P, qf[nb], v ? t : 0, g * P.G + (v ? hh : 0), v);
+    state_init(st[nb]);
+  }
+  const bool wave_live = __any(live[0] || live[1]);
+
+  const int32_t* ptrow = P.pt + (int64_t)first * P.pt_stride;
+  // 512 cg <= nh: every shared page is in the first member's table row
+  const int nh = (int)min<int64_t>(P.ctx[first], (int64_t)P.pt_stride * kPage);
+  const int kt0 = k * kTilesPerSplit, ntiles = kTilesPerSplit;
+  auto fetch = [&](int kt, int buf) {
+    int64_t pb[kPagesPerTile];
+#pragma unroll
+    for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt * kPagesPerTile + b, nh, g);
+#pragma unroll
+    for (int w = 0; w < WCH; ++w) {
+      const int q = wave * WCH + w;
+      const int blk = q / (BLK / 512), sub = q % (BLK / 512);
+      const int b = blk % kPagesPerTile;
+      const int64_t pbb = pb[b] < 0 ? 0 : pb[b];
+      const uint16_t* src =
+          block_ptr<D>(blk < kPagesPerTile ? P.kpool : P.vpool, pbb) + 512 * sub + 8 * lane;
+      const uint32_t dst = (uint32_t)(uintptr_t)(lds + (buf * NBLK + blk) * BLK + 512 * sub);
+      lds_dma16(src, uni((int)dst));
+    }
+  };
+  // a page id outside the pool reads as zeros, as on the split path
+  auto pages_ok = [&](int kt) {
+    bool ok = true;
+#pragma unroll
+    for (int b = 0; b < kPagesPerTile; ++b)
+      ok = ok && page_block(P, ptrow, kt * kPagesPerTile + b, nh, g) >= 0;
+    return ok;
+  };
+  auto zero_pages = [&](int kt, int buf) {
+    bool pvalid[kPagesPerTile];
+#pragma unroll
+    for (int b = 0; b < kPagesPerTile; ++b)
+      pvalid[b] = page_block(P, ptrow, kt * kPagesPerTile + b, nh, g) >= 0;
+    for (int ch = threadIdx.x; ch < TILE / 8; ch += 256) {
+      const int blk = ch / (BLK / 8);
+      if (!pvalid[blk % kPagesPerTile])
+        *reinterpret_cast<u16x8*>(lds + (buf * NBLK + blk) * BLK + (ch % (BLK / 8)) * 8) = zero8();
+    }
+  };
+
+  wait_vmcnt<0>();  // the Q operands are in registers before any tile copy is issued
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t) fetch(kt0 + t, t % STAGES);
+  for (int it = 0; it < ntiles; ++it) {
+    const int kt = kt0 + it;
+    const int j0 = kt * kTileKeys;
+    const int buf = it % STAGES;
+    const int later = min(STAGES - 2, ntiles - 1 - it);
+    if (later >= 3)
+      wait_vmcnt<3 * WCH>();
+    else if (later == 2)
+      wait_vmcnt<2 * WCH>();
+    else if (later == 1)
+      wait_vmcnt<WCH>();
+    else
+      wait_vmcnt<0>();
+    lds_barrier();  // every wavefront's part of tile kt is in LDS; tile kt - 1 is consumed
+    if (!pages_ok(kt)) {
+      zero_pages(kt, buf);
+      lds_barrier();
+    }
+    if (it + STAGES - 1 < ntiles) fetch(kt + STAGES - 1, (it + STAGES - 1) % STAGES);
+    const uint16_t* T = lds + buf * NBLK * BLK;
+    if (wave_live) {
+      f32x4 acc[NB][kPagesPerTile];
+      tile_scores<D, NB>(
+          [&](int b, int ks) { return *reinterpret_cast<const u16x8*>(T + b * BLK + 512 * ks + 8 * lane); },
+          qf, acc);
+      // every key of a shared split is visible to every member column
+      TileWeights w[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D, false, false>(st[nb], acc[nb], j0, 0, 0, P.c);
+#pragma unroll
+      for (int m = 0; m < D / 16; ++m) {
+        const int o = 256 * m + 4 * lane;
+        const u16x8 v0 = cat4(*reinterpret_cast<const u16x4*>(T + 4 * BLK + o),
+                              *reinterpret_cast<const u16x4*>(T + 5 * BLK + o));
+        const u16x8 v1 = cat4(*reinterpret_cast<const u16x4*>(T + 6 * BLK + o),
+                              *reinterpret_cast<const u16x4*>(T + 7 * BLK + o));
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) tile_pv_block<D>(st[nb], w[nb], m, v0, v1);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) tile_commit<D>(st[nb], w[nb]);
+    }
+  }
+
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    if (!live[nb]) continue;
+    if (grp == 0) {
+      P.ws_m[pidx[nb]] = st[nb].m;
+      P.ws_z[pidx[nb]] = st[nb].z;
+    }
+    float* u = P.ws_u + pidx[nb] * D + 4 * grp;
+#pragma unroll
+    for (int m = 0; m < D / 16; ++m) *reinterpret_cast<f32x4*>(u + 16 * m) = st[nb].u[m];
+  }
+}
+
+// Items: KV head major, then listed group, then (tile, split).  Each XCD
+// (workgroup id mod 8) takes a contiguous eighth of the list, which its
+// workgroups run in turn: the grid is sized to the chip, not to the list.
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefix_kernel(Params P) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];  // [STAGES][8 page blocks]
+  __shared__ int scu[kChunkCols + 1];  // cu of the requests an item's rows may belong to
+  const int ngroups = P.casc_hdr[0], per_head = P.casc_hdr[1];
+  if (ngroups < 1 || ngroups > P.num_seqs / 2 || per_head < 1 || per_head > (1 << 24)) return;
+  const int total = per_head * P.hkv;
+  const int per_xcd = (total + 7) / 8;
+  for (int j = (int)(blockIdx.x / 8); j < per_xcd; j += (int)(gridDim.x / 8)) {
+    const int i = uni((int)(blockIdx.x % 8) * per_xcd + j);
+    if (i >= total) break;
+    prefix_item<D>(P, i, ngroups, per_head, lds, scu);
+    __syncthreads();  // LDS (ring, scu) is free for the next item
+  }
+}
+
+// ---------------------------------------------------------------------------
 // KV write: one thread per (token, KV head, 8 consecutive d)
 template <int D>
 __global__ __launch_bounds__(256) void kv_write_kernel(const uint16_t* knew, const uint16_t* vnew,
@@ -1387,22 +1835,30 @@ size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 
 struct WsLayout {
-  size_t off_full, off_part, off_chunk, items, m_off, z_off, u_off, total;
+  size_t off_full, off_part, off_chunk, casc_hdr, casc_seq, casc_off, casc_grp, items, m_off,
+      z_off, u_off, total;
 };
 
-// Workspace: three offset arrays of num_seqs + 1 int32, the split work list
-// (8 int32 per grid slot of the split launch), then the split partial states
+// Workspace: three offset arrays of num_seqs + 1 int32, the shared-prefix
+// plan (a header, one int32 per request, and per listed group -- at most
+// num_seqs / 2 -- an item offset and 4 int32), the split work list (8 int32
+// per (request, KV head, split, column half)), then the split partial states
 // (m, z, U) for every (request, KV head, column < 32, split).
 WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_context_len) {
   const int64_t ms = ((int64_t)max_context_len + kSplitKeys - 1) / kSplitKeys;
   const int64_t n = (int64_t)num_seqs * h->hkv * kSplitCols * (ms < 1 ? 1 : ms);
   const size_t offs = round_up((size_t)(num_seqs + 1) * sizeof(int32_t));
+  const size_t groups = (size_t)num_seqs / 2 + 1;
   WsLayout L;
   L.off_full = 0;
   L.off_part = offs;
   L.off_chunk = 2 * offs;
-  L.items = 3 * offs;
-  L.m_off = L.items + round_up((size_t)num_seqs * h->hkv * (ms < 1 ? 1 : ms) * kItemInts * sizeof(int32_t));
+  L.casc_hdr = 3 * offs;
+  L.casc_seq = L.casc_hdr + 256;
+  L.casc_off = L.casc_seq + offs;
+  L.casc_grp = L.casc_off + round_up((groups + 1) * sizeof(int32_t));
+  L.items = L.casc_grp + round_up(groups * 4 * sizeof(int32_t));
+  L.m_off = L.items + round_up((size_t)num_seqs * h->hkv * (ms < 1 ? 1 : ms) * 2 * kItemInts * sizeof(int32_t));
   L.z_off = L.m_off + round_up(n * sizeof(float));
   L.u_off = L.z_off + round_up(n * sizeof(float));
   L.total = L.u_off + round_up((size_t)n * h->d * sizeof(float));
@@ -1438,10 +1894,18 @@ bool fuses_write(const vd_attn* h, const vd_attn_batch* b) {
          b->max_q_len <= kMaxNewRows;
 }
 
-// The plan launch runs for the work lists of a call with more requests, and
-// for new tokens the split items do not write.
+// The shared-prefix pass runs for calls with the shared_pages hint: at most
+// kCascMaxSeqs requests, no sliding window, contexts of more than one split.
+bool cascades(const vd_attn* h, const vd_attn_batch* b) {
+  return b->shared_pages != 0 && h->window == 0 && b->num_seqs >= 2 &&
+         b->num_seqs <= kCascMaxSeqs && b->max_context_len > kSplitKeys &&
+         b->total_q_tokens * h->group <= INT32_MAX;
+}
+
+// The plan launch runs for the work lists of a call with more requests, for
+// new tokens the split items do not write, and for the shared-prefix plan.
 bool needs_plan(const vd_attn* h, const vd_attn_batch* b) {
-  return !plans_inwave(b) || (b->k_new != nullptr && !fuses_write(h, b));
+  return !plans_inwave(b) || (b->k_new != nullptr && !fuses_write(h, b)) || cascades(h, b);
 }
 
 int split_nb(const vd_attn* h, int32_t max_q_len) {
@@ -1484,6 +1948,11 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.inwave = plans_inwave(b);
   P.lse = b->lse;
   P.fuse_write = fuses_write(h, b);
+  P.casc = cascades(h, b);
+  P.casc_hdr = reinterpret_cast<int32_t*>(w + L.casc_hdr);
+  P.casc_seq = reinterpret_cast<int32_t*>(w + L.casc_seq);
+  P.casc_off = reinterpret_cast<int32_t*>(w + L.casc_off);
+  P.casc_grp = reinterpret_cast<int4*>(w + L.casc_grp);
   return P;
 }
 
@@ -1505,26 +1974,60 @@ int run_plan(const Params& P, hipStream_t s) {
 // optional timing events e0 / e1 with the dispatch itself.
 template <int D, bool NT>
 auto split_kernel_for(const Params& P) {
-  // a handle's window is fixed at creation: one kernel per handle and width
-  const bool win = P.window > 0;
-  return P.split_cols == 16 ? (win ? &split_kernel<D, 1, true, NT> : &split_kernel<D, 1, false, NT>)
-                            : (win ? &split_kernel<D, 2, true, NT> : &split_kernel<D, 2, false, NT>);
+  // a handle's window is fixed at creation: one kernel per handle
+  return P.window > 0 ? &split_kernel<D, true, NT> : &split_kernel<D, false, NT>;
 }
 
 template <int D>
 int run_splits(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e0 = nullptr,
                hipEvent_t e1 = nullptr) {
-  // upper bound of the split items; workgroups past the call's items exit at
-  // once.  Workgroups that plan for themselves take XCD-contiguous ranges of
-  // the items, so their count is a multiple of the 8 XCDs; with a work list
-  // there is exactly one workgroup per list entry.
-  int64_t items = (int64_t)P.num_seqs * P.hkv * P.max_splits;
-  if (P.inwave) items = (items + 7) / 8 * 8;
+  // upper bound of the split items (the work-list length); a workgroup stops
+  // at its first slot past the call's items.  Workgroups that plan for
+  // themselves take XCD-contiguous ranges of the items.
+  const int64_t items = split_slots(P);
   if (items > INT32_MAX - 8) return VD_ERR_INVALID_ARG;
-  const dim3 grid((unsigned)items), block(64);
+  // at most about twice the wavefronts the chip holds at once (1024 SIMDs,
+  // two wavefronts each); a multiple of 8
+  const int64_t cap = 4096;
+  const dim3 grid((unsigned)((std::min(items, cap) + 7) / 8 * 8)), block(64);
   const auto kern = stream_kv ? split_kernel_for<D, true>(P) : split_kernel_for<D, false>(P);
   hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, P);
   return launched();
+}
+
+template <int D>
+int run_prefix(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr) {
+  // Two workgroups per CU (256 CUs), or fewer for fewer items: an upper
+  // bound of the items is Hkv (ceil(T G / 128) + B / 2) tiles (the members'
+  // query rows of different groups are disjoint, and a listed group has at
+  // least two requests) times the shared splits, at most max_splits - 1.
+  // A multiple of the 8 XCDs.
+  const int64_t bound = (int64_t)P.hkv *
+                        ((P.T * P.G + kChunkCols - 1) / kChunkCols + P.num_seqs / 2) *
+                        std::min(kCascMaxSplits, std::max(P.max_splits - 1, 1));
+  const int64_t blocks = (std::min<int64_t>(bound, 2 * 256) + 7) / 8 * 8;
+  constexpr size_t lds = chunk_lds_bytes<D>();
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&prefix_kernel<D>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)lds);
+  if (attr != hipSuccess) return VD_ERR_LAUNCH;
+  hipExtLaunchKernelGGL((prefix_kernel<D>), dim3((unsigned)blocks), dim3(256), (uint32_t)lds, s, e0,
+                        nullptr, 0, P);
+  return launched();
+}
+
+// The splits phase: the shared-prefix kernel (calls with the shared_pages
+// hint), then the split kernel; e0 / e1 are recorded by the first and the last
+// launch.
+template <int D>
+int run_split_phase(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e0 = nullptr,
+                    hipEvent_t e1 = nullptr) {
+  if (P.casc) {
+    const int rc = run_prefix<D>(P, s, e0);
+    if (rc != VD_OK) return rc;
+    return run_splits<D>(P, stream_kv, s, nullptr, e1);
+  }
+  return run_splits<D>(P, stream_kv, s, e0, e1);
 }
 
 template <int D>
@@ -1633,8 +2136,10 @@ int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* out, 
   if (!out) return VD_ERR_INVALID_ARG;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
-  const bool nt = b->shared_pages == 0;
-  return h->d == 64 ? run_splits<64>(P, nt, stream) : run_splits<128>(P, nt, stream);
+  // with the shared-prefix pass, the shared splits are read (cached) by the
+  // shared-prefix kernel and the split items stream the requests' own pages
+  const bool nt = b->shared_pages == 0 || P.casc;
+  return h->d == 64 ? run_split_phase<64>(P, nt, stream) : run_split_phase<128>(P, nt, stream);
 }
 
 int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* b, void* out,
@@ -1664,9 +2169,11 @@ int vd_attn_forward_splits_timed(const vd_attn* h, const vd_attn_batch* b, void*
   if (!out) return VD_ERR_INVALID_ARG;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
-  const bool nt = b->shared_pages == 0;
-  return h->d == 64 ? run_splits<64>(P, nt, stream, start, stop)
-                    : run_splits<128>(P, nt, stream, start, stop);
+  // with the shared-prefix pass, the shared splits are read (cached) by the
+  // shared-prefix kernel and the split items stream the requests' own pages
+  const bool nt = b->shared_pages == 0 || P.casc;
+  return h->d == 64 ? run_split_phase<64>(P, nt, stream, start, stop)
+                    : run_split_phase<128>(P, nt, stream, start, stop);
 }
 
 int vd_attn_forward_chunks_timed(const vd_attn* h, const vd_attn_batch* b, void* out,
