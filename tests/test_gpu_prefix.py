@@ -1,8 +1,9 @@
 """GPU tests of the shared-prefix pass (calls with the shared_pages hint): the
 plan launch finds adjacent requests whose page tables start with the same
 pages, and the shared-prefix kernel computes their shared 512-key splits once
-for all their rows; the merge continues from the folded state.  Its output
-must be bit-identical to the same call without the pass (every split read by
+for all their rows, storing the partial states the rows' own split items would
+have stored; the merge folds them with the rest.  Its output must be
+bit-identical to the same call without the pass (every split read by
 the request's own split items) and to a call with copied prefix pages, and
 within tolerance of the oracle."""
 from __future__ import annotations
@@ -122,11 +123,21 @@ def test_prefix_lse():
 
 def test_prefix_deep():
     """A 36-split shared prefix: the pass covers its first 32 splits, the split
-    items the rest, and the long merge (more than 16 splits) continues from
-    the folded state."""
+    items the rest, and the long merge (more than 16 splits) folds them all."""
     call = W.config5(num_req=4, prefix=36 * 512, suf_lo=100, suf_hi=600, shape=W.LLAMA70B)
     a_bits = U.gpu_run(call, shared_pages=True)
     a = U.by_position(call, a_bits)
     U.assert_same_bits(a, U.by_position(call, U.gpu_run(call, shared_pages=False)),
                        min_common=call.total_q_tokens)
     U.say("  deep prefix: %s" % U.parity(call, a_bits))
+
+
+def test_prefix_full_size_verify():
+    """The 70B prefix-shared verify batch at full size (256 requests on a
+    2048-token prefix, s = 4 / 1), in the launch configuration the benchmark
+    times: every row bit-identical with and without the pass."""
+    call = W.config5()
+    with_pass = U.by_position(call, U.gpu_run(call, poison=False, shared_pages=True))
+    without = U.by_position(call, U.gpu_run(call, poison=False, shared_pages=False))
+    U.say("  full cfg5: %d rows compared" % U.assert_same_bits(with_pass, without,
+                                                              min_common=call.total_q_tokens))
