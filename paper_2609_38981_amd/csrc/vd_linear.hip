@@ -15,15 +15,16 @@
 // computes a row, nor the other rows of the call reach its bits; only K (the
 // chain length and order) does, and there is no split over K.
 //
-// Launch: one workgroup of 4 wavefronts per 128 x 128 output tile, each
-// wavefront a 64 x 64 quarter (4 x 4 MFMA blocks of 16 x 16).  K advances in
-// steps of 64 through a 2-stage LDS ring of A and B tiles (128 rows x 64
-// values each) filled by direct global-to-LDS copies; the 16-byte chunks of
-// each 128-byte LDS row are XOR-swizzled by the row so that the 16 rows one
-// operand read touches fall in different banks.  Tiles are taken in groups of
-// 4 row tiles sweeping the column tiles, and each XCD (workgroup id mod 8)
-// takes a contiguous range of that order, so the A and B panels of its
-// workgroups are shared in its L2.
+// Launch: one workgroup of 8 wavefronts (4 x 2) per 256 x 192 output tile,
+// each wavefront a 64 x 96 part (4 x 6 MFMA blocks of 16 x 16).  K advances
+// in steps of 64 through a 2-stage LDS ring of A and B tiles (256 and 192
+// rows x 64 values; 112 KB, one workgroup and two wavefronts per SIMD on a
+// CU) filled by direct global-to-LDS copies; the 16-byte chunks of each
+// 128-byte LDS row are XOR-swizzled by the row so that the 16 rows one operand
+// read touches fall in different banks.  Tiles are taken in groups of 4 row
+// tiles sweeping the column tiles, and each XCD (workgroup id mod 8) takes a
+// contiguous range of that order, so the A and B panels of its workgroups are
+// shared in its L2.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -36,13 +37,19 @@ using namespace vd;
 
 namespace {
 
-// Tile configuration: each of the 4 wavefronts (2 x 2) computes kXB x kYB MFMA
+// Tile configuration: kWM x kWN wavefronts, each computing kXB x kYB MFMA
 // blocks of 16 x 16; K advances kBK per step (kBK / 32 MFMA chunks).  On the
-// Llama-3-8B QKV shape, 4 x 4 blocks with 64-wide steps (two workgroups per
-// CU) ran faster than 4 x 8 or 8 x 4 blocks with 32- or 64-wide steps.
-constexpr int kXB = 4, kYB = 4, kBK = 64;
-constexpr int kBM = 2 * 16 * kXB;           // rows of a (tokens) per workgroup tile
-constexpr int kBN = 2 * 16 * kYB;           // rows of b (output features) per workgroup tile
+// Llama-3-8B QKV shape, 4 x 2 wavefronts of 4 x 6 blocks (a 256 x 192 tile,
+// one workgroup per CU) ran 9% faster than 2 x 2 wavefronts of 4 x 4 blocks
+// (128 x 128, two workgroups per CU), which beat 4 x 8 or 8 x 4 blocks per
+// wavefront at 4 wavefronts, 2 x 4 / 4 x 2 wavefronts of 4 x 4, 4 x 8 or
+// 8 x 4 blocks, and 192 x 256 tiles.
+constexpr int kWM = 4, kWN = 2;
+constexpr int kXB = 4, kYB = 6, kBK = 64;
+constexpr int kWaves = kWM * kWN;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kBM = kWM * 16 * kXB;         // rows of a (tokens) per workgroup tile
+constexpr int kBN = kWN * 16 * kYB;         // rows of b (output features) per workgroup tile
 constexpr int kRowBytes = kBK * 2;          // one staged row of a tile
 constexpr int kChunks = kRowBytes / 16;     // 16-byte chunks per staged row
 constexpr int kRowsPerCopy = 1024 / kRowBytes;
@@ -50,9 +57,10 @@ constexpr int kGroupM = 4;                  // row tiles per group of the tile o
 constexpr int kTileA = kBM * kRowBytes, kTileB = kBN * kRowBytes;
 constexpr int kStageBytes = kTileA + kTileB;
 constexpr int kLinLds = 2 * kStageBytes;    // 2-stage ring
-constexpr int kCopiesA = kTileA / 1024 / 4, kCopiesB = kTileB / 1024 / 4;  // per wavefront
+constexpr int kCopiesA = kTileA / 1024 / kWaves, kCopiesB = kTileB / 1024 / kWaves;  // per wavefront
 static_assert(kChunks == 4 || kChunks == 8, "staged rows of 64 or 128 bytes");
-static_assert(kCopiesA * 4096 == kTileA && kCopiesB * 4096 == kTileB, "copy split");
+static_assert(kCopiesA * 1024 * kWaves == kTileA && kCopiesB * 1024 * kWaves == kTileB,
+              "copy split");
 
 // Swizzle key of staged row r: chunk ch of the row sits in 16-byte slot
 // ch ^ key(r), so that 8 consecutive rows read at one chunk fill 8 distinct
@@ -64,7 +72,7 @@ __device__ __forceinline__ int swz(int r, int ch) {
   return r * kRowBytes + ((ch ^ swz_key(r)) << 4);
 }
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void linear_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void linear_kernel(
     const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, uint16_t* c, int64_t ldc,
     int64_t M, int N, int K, int tiles_m, int tiles_n) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
@@ -85,7 +93,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int64_t m0 = (first_m + in_group % size_m) * kBM;
   const int n0 = (in_group / size_m) * kBN;
 
-  // Copies: the staged A tile is kCopiesA * 4 copies of 1 KB (kRowsPerCopy
+  // Copies: the staged A tile is kCopiesA * kWaves copies of 1 KB (kRowsPerCopy
   // rows each), wavefront w taking copies w * kCopiesA + j; the same for B.
   // Lane l of a copy carries row l / kChunks of it and 16-byte slot
   // l % kChunks, i.e. source chunk slot ^ key(row) (the copy's first row is a
@@ -119,8 +127,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       lds_dma16(bsrc[j] + k0, uni((int)(st + kTileA + 1024 * (wave * kCopiesB + j))));
   };
 
-  // this wavefront's quarter: rows wm .. wm + 16 kXB - 1, columns wn .. wn + 16 kYB - 1
-  const int wm = 16 * kXB * (wave >> 1), wn = 16 * kYB * (wave & 1);
+  // this wavefront's part: rows wm .. wm + 16 kXB - 1, columns wn .. wn + 16 kYB - 1
+  const int wm = 16 * kXB * (wave / kWN), wn = 16 * kYB * (wave % kWN);
   const int col = lane & 15, grp = lane >> 4;
   f32x4 acc[kXB][kYB];
 #pragma unroll
@@ -195,7 +203,7 @@ extern "C" int vd_linear(const void* a, int64_t lda, const void* b, int64_t ldb,
       reinterpret_cast<const void*>(&linear_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
       kLinLds);
   if (attr != hipSuccess) return VD_ERR_LAUNCH;
-  hipLaunchKernelGGL(linear_kernel, dim3((unsigned)blocks), dim3(256), kLinLds, stream,
+  hipLaunchKernelGGL(linear_kernel, dim3((unsigned)blocks), dim3(kThreads), kLinLds, stream,
                      static_cast<const uint16_t*>(a), lda, static_cast<const uint16_t*>(b), ldb,
                      static_cast<uint16_t*>(c), ldc, M, N, K, (int)tiles_m, (int)tiles_n);
   return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH;
