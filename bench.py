@@ -60,21 +60,34 @@ def workloads():
     }
 
 
+def kernel_code_digest() -> str:
+    """SHA-256 of the attention kernels' code: the sources with comments
+    removed and whitespace collapsed, so that an edit of a comment does not
+    count as a change of the kernel."""
+    import hashlib
+    import re
+
+    csrc = os.path.join(ROOT, "paper_2609_38981_amd", "csrc")
+    code = []
+    for n in ("vd_attn.hip", "vd_cas.hpp", "vd_hw.hpp"):
+        with open(os.path.join(csrc, n)) as f:
+            t = f.read()
+        t = re.sub(r"/\*.*?\*/", " ", t, flags=re.S)
+        t = re.sub(r"//[^\n]*", " ", t)
+        code.append(" ".join(t.split()))
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()
+
+
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary
-    (profiles/hbm_traffic.json), or None when the kernel sources changed since
+    (profiles/hbm_traffic.json), or None when the kernels' code changed since
     the counters were taken or no summary covers this kernel and workload."""
-    import hashlib
-
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
-    csrc = os.path.join(ROOT, "paper_2609_38981_amd", "csrc")
-    src = b"".join(open(os.path.join(csrc, n), "rb").read()
-                   for n in ("vd_attn.hip", "vd_cas.hpp", "vd_hw.hpp"))
-    if d.get("source_sha256") != hashlib.sha256(src).hexdigest():
+    if d.get("code_sha256") != kernel_code_digest():
         return None
     if d.get("kernel") != kernel or d.get("workload") != workload:
         return None

@@ -1,19 +1,28 @@
 // vd_attn.hip -- HIP kernels for gfx950 and the C ABI of libvdattn.so.
 //
 // Kernels of one attention call, all on the caller's stream:
-//   plan kernel   one workgroup; reads the per-request lengths and writes
-//                 prefix offsets of the compact work lists, and the split
-//                 work list itself, into the workspace, so that no launched
-//                 wavefront is idle in the middle of the grid (no
-//                 device-to-host synchronisation).  Its other workgroups
-//                 write the call's new tokens into the pool.
-//   split kernel  one wavefront (workgroup) per (request, KV head, 512-key split) for
-//                 requests with at most 32 query-head rows per KV head
-//                 (decode, verify).  K/V go straight from HBM to registers
-//                 in the matrix-core operand layout; writes a partial state.
-//                 Whole 512-key splits are listed before the shorter last
-//                 splits, and those by decreasing length, so the shortest
-//                 items fill the end of the launch.
+//   plan kernel   launched only when needed (more than 256 requests, new
+//                 tokens the split items do not write, or the shared_pages
+//                 hint).  Workgroup 0 reads the per-request lengths and
+//                 writes the split work list and, with the hint, the
+//                 shared-prefix plan (groups of adjacent requests whose page
+//                 tables share leading splits) into the workspace, with no
+//                 device-to-host synchronisation; its other workgroups write
+//                 the call's new tokens into the pool.  Without a plan
+//                 launch, the split and chunk workgroups derive their items
+//                 from the lengths themselves.
+//   prefix kernel one workgroup (4 wavefronts x 32 columns) per (KV head,
+//                 listed group, 128 query-head rows of its members, shared
+//                 split): each shared split is read once for all member rows;
+//                 writes the same partial states their split items would.
+//   split kernel  one wavefront (workgroup) per (request, KV head, 512-key
+//                 split, 16 query-head rows) for requests with at most 32
+//                 query-head rows per KV head (decode, verify).  K/V go
+//                 straight from HBM to registers in the matrix-core operand
+//                 layout; writes a partial state.  Whole 512-key splits are
+//                 listed before the shorter last splits, and those by
+//                 decreasing length, so the shortest items fill the end of
+//                 the launch.
 //   chunk kernel  one workgroup (4 wavefronts x 32 columns) per (request,
 //                 KV head, 128 query-head rows) for longer chunks (prefill);
 //                 K/V tiles are staged in LDS and shared by the wavefronts;
