@@ -233,6 +233,10 @@ __device__ __forceinline__ void kv_write_one(const uint16_t* knew, const uint16_
              *reinterpret_cast<const u16x8*>(vnew + src));
 }
 
+// Calls of at most this many requests find a row's request with one load of
+// all the lengths instead of a search.
+constexpr int kAppendInWaveSeqs = 256;
+
 // Writes the K/V of the call's query rows (every KV head) at the slots their
 // positions have in the request's page table.  The wavefront of query row t
 // writes the rows of t's 4-slot group (positions p .. up to the next multiple
@@ -242,15 +246,48 @@ __device__ __forceinline__ void kv_write_one(const uint16_t* knew, const uint16_
 template <int D>
 __device__ __forceinline__ void append_rows(const Params& P, int64_t t) {
   if (t >= P.T) return;
-  const int r = find_req(P.cu, P.num_seqs, (int)t);
-  const Req R = load_req(P, r);
+  int r;
+  Req R;
+  if (P.num_seqs <= kAppendInWaveSeqs) {
+    // one round trip: lane l holds the lengths of requests l, 64 + l, ...;
+    // row t belongs to the request after every request that ends at or
+    // before it
+    constexpr int C = kAppendInWaveSeqs / 64;
+    const int lane = __lane_id();
+    int cq0[C], cq1[C], cn[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const int rr = min(64 * c + lane, P.num_seqs - 1);
+      cq0[c] = P.cu[rr];
+      cq1[c] = P.cu[rr + 1];
+      cn[c] = P.ctx[rr];
+    }
+    r = 0;
+#pragma unroll
+    for (int c = 0; c < C; ++c) r += __popcll(__ballot(64 * c + lane < P.num_seqs && cq1[c] <= t));
+    r = uni(r);
+    if (r >= P.num_seqs) return;
+    int q0 = 0, q1 = 0, n = 0;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      if (c == r / 64) {
+        q0 = __builtin_amdgcn_readlane(cq0[c], r % 64);
+        q1 = __builtin_amdgcn_readlane(cq1[c], r % 64);
+        n = __builtin_amdgcn_readlane(cn[c], r % 64);
+      }
+    R = make_req(P, q0, q1, n);
+  } else {
+    r = find_req(P.cu, P.num_seqs, (int)t);
+    R = load_req(P, r);
+  }
   if (!R.valid || t < R.q0 || t >= (int64_t)R.q0 + R.s) return;
   const int p0 = R.n - R.s;
   const int p = p0 + (int)(t - R.q0);
   if (p != p0 && (p & 3) != 0) return;  // written by the wavefront of its group's first row
   const int cnt = min(R.n, (p & ~3) + 4) - p;  // rows t .. t + cnt - 1
-  const int32_t page = P.pt[(int64_t)r * P.pt_stride + p / kPage];
-  if (page < 0 || page >= P.num_pages) return;
+  // the page id is loaded with the first batch of K rows (one round trip)
+  const int32_t* pte = P.pt + (int64_t)r * P.pt_stride + p / kPage;
+  int32_t page = -1;
   const int slot0 = p % kPage;
   const int lane = __lane_id();
   const int64_t rs = (int64_t)P.hkv * D;  // elements per row of k_new / v_new
@@ -270,6 +307,10 @@ __device__ __forceinline__ void append_rows(const Params& P, int64_t t) {
         const int i = x / (P.hkv * (D / 8)), hd = x % (P.hkv * (D / 8));
         v[u] = *reinterpret_cast<const u16x8*>(P.knew + (t + i) * rs + hd * 8);
       }
+    }
+    if (x0 == 0) {
+      page = *pte;
+      if (page < 0 || page >= P.num_pages) return;
     }
 #pragma unroll
     for (int u = 0; u < B; ++u) {
