@@ -267,6 +267,7 @@ def main():
     import torch
 
     from paper_2609_38981_amd import staging as S
+    from paper_2609_38981_amd import vdattn as V
 
     torch.cuda.set_device(0)
     if args.workload in LINEAR_WORKLOADS:
@@ -393,7 +394,7 @@ def main():
         # (no window, 2 .. 1024 requests, contexts past one split): the timed
         # phase is the shared-prefix kernel and the split kernel together
         casc = bool(reps[0][0].batch.shared_pages) and sh.window == 0 and \
-            2 <= call.num_seqs <= 1024 and call.max_context_len > 512
+            2 <= call.num_seqs <= 1024 and call.max_context_len > V.SPLIT_KEYS
         roof = {"kernel": "prefix_kernel+split_kernel" if casc else "split_kernel",
                 "bound": "hbm", "achieved": round(ach, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),

@@ -23,7 +23,7 @@
  * requests of the call, their order, the page table (physical placement,
  * stride, sharing of pages between requests), num_pages, the hints, the
  * workspace contents or the stream.  Keys are processed in tiles of 64
- * logical positions and in splits of 512 logical positions whose partial
+ * logical positions and in splits of 1024 logical positions whose partial
  * states are merged in ascending split order; both sizes are fixed by the
  * handle, never by the batch.
  *
@@ -125,7 +125,7 @@ typedef struct {
   /* HOST hint, never value-relevant: nonzero when some pages are read by several requests
    * of the call (a shared prefix, Section 4.1's prefix cache).  It turns on the shared-prefix
    * pass: the plan launch compares the page tables of adjacent requests and finds groups of
-   * requests whose tables start with the same pages (requests r - 1 and r share 512-key
+   * requests whose tables start with the same pages (requests r - 1 and r share 1024-key
    * split k when their entries of splits 0 .. k are equal; a group shares the splits all its
    * neighbours share, at most 32).  Each shared split is then read once for the query rows
    * of every member (a request of the group with s_r * (Hq / Hkv) <= 32 whose rows all lie
@@ -146,8 +146,8 @@ typedef struct {
 /* Bytes of workspace one call needs for the given host-side sizes: the plan
  * (int32 arrays of about 3 num_seqs, the shared-prefix list and the split work
  * list) and, for every
- * (request, KV head, query-head row < 32, 512-key split < ceil(max_context_len /
- * 512)), a partial state of head_dim + 2 floats. */
+ * (request, KV head, query-head row < 32, 1024-key split < ceil(max_context_len /
+ * 1024)), a partial state of head_dim + 2 floats. */
 int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
                            int32_t max_context_len, size_t* bytes);
 
@@ -171,7 +171,7 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, voi
  *           work lists of the split and shared-prefix phases into the
  *           workspace (no device-to-host synchronisation);
  *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
- *           per (request, KV head, 512-key split, 16 query-head rows), after
+ *           per (request, KV head, 1024-key split, 16 query-head rows), after
  *           the shared-prefix items (shared_pages hint) -- one per (group, KV
  *           head, 128 query-head rows of its members, shared split).  Without
  *           a plan launch, every workgroup derives its items from the lengths
@@ -253,7 +253,7 @@ int vd_linear(const void* a, int64_t lda, const void* b, int64_t ldb, void* c, i
 const char* vd_status_string(int status);
 
 /* Fixed tiling constants of a handle (host query, for reports and tests):
- * tile_keys = 64, split_keys = 512, page_size = 16. */
+ * tile_keys = 64, split_keys = 1024, page_size = 16. */
 int vd_attn_tiling(const vd_attn* h, int32_t* tile_keys, int32_t* split_keys,
                    int32_t* page_size);
 

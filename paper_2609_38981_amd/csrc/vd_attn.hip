@@ -15,11 +15,11 @@
 //                 listed group, 128 query-head rows of its members, shared
 //                 split): each shared split is read once for all member rows;
 //                 writes the same partial states their split items would.
-//   split kernel  one wavefront (workgroup) per (request, KV head, 512-key
+//   split kernel  one wavefront (workgroup) per (request, KV head, 1024-key
 //                 split, 16 query-head rows) for requests with at most 32
 //                 query-head rows per KV head (decode, verify).  K/V go
 //                 straight from HBM to registers in the matrix-core operand
-//                 layout; writes a partial state.  Whole 512-key splits are
+//                 layout; writes a partial state.  Whole 1024-key splits are
 //                 listed before the shorter last splits, and those by
 //                 decreasing length, so the shortest items fill the end of
 //                 the launch.
@@ -450,7 +450,7 @@ __device__ __forceinline__ bool run_start(int key) {
 //    shares c = the smallest sh of the run.  An invalid request is a group of
 //    its own, so the query rows of a group's requests are consecutive.
 //  * A member is a request of a group on the split path whose query rows all
-//    lie past the c shared splits (n - s >= 512 c): each of its rows sees
+//    lie past the c shared splits (n - s >= 1024 c): each of its rows sees
 //    every key of them, and none of them is a new token of the call.
 //  * A group with at least two members is listed: its members' splits
 //    0 .. c - 1 are computed by the shared-prefix kernel (csq[r] = c), their
@@ -459,7 +459,7 @@ __device__ __forceinline__ bool run_start(int key) {
 // Requires num_seqs <= kCascMaxSeqs and 1024 threads.  One round trip to
 // memory: the lengths and every page-table entry compared are loaded
 // together (the comparison runs over the first E entries of every row,
-// E = 32 * min(kCascMaxSplits, max_context_len / 512) within the table stride,
+// E = 64 * min(kCascMaxSplits, max_context_len / 1024) within the table stride,
 // and is cut to the pair's own contexts afterwards).
 template <int W>  // entries per load: 1, or 4 for a 16-byte aligned table
 __device__ __forceinline__ void compare_rows(const Params& P, int B, int E, int* fd) {
@@ -1022,7 +1022,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 // Split items without a plan launch (calls of at most kInWaveMaxSeqs
 // requests): every workgroup reads all requests' lengths in one round trip
 // (lane l holds requests l, 64 + l, ...) and derives its own item.  Items are
-// listed per KV head -- every whole 512-key split (requests ascending, splits
+// listed per KV head -- every whole 1024-key split (requests ascending, splits
 // ascending), then every last partial split, longest first (tile count 8 down
 // to 1, requests ascending) -- and each XCD (workgroup id mod 8) takes a
 // contiguous range of the list: with 8 KV heads XCD x runs head x, so a page
@@ -1738,7 +1738,7 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
   const bool wave_live = __any(live[0] || live[1]);
 
   const int32_t* ptrow = P.pt + (int64_t)first * P.pt_stride;
-  // 512 cg <= nh: every shared page is in the first member's table row
+  // 1024 cg <= nh: every shared page is in the first member's table row
   const int nh = (int)min<int64_t>(P.ctx[first], (int64_t)P.pt_stride * kPage);
   const int kt0 = k * kTilesPerSplit, ntiles = kTilesPerSplit;
   auto fetch = [&](int kt, int buf) {

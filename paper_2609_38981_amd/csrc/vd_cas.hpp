@@ -11,9 +11,9 @@
 //
 // Tiling (fixed per handle, never chosen from the batch):
 //   * key tile     = 64 logical positions = 4 pages of 16
-//   * split        = 512 logical positions (8 tiles); split k covers keys
-//                    [512k, 512k + 512); a row at position p has
-//                    ceil((p + 1) / 512) splits
+//   * split        = 1024 logical positions (16 tiles); split k covers keys
+//                    [1024k, 1024k + 1024); a row at position p has
+//                    ceil((p + 1) / 1024) splits
 //   * dot products = v_mfma_f32_16x16x32_bf16, keys in the M dimension and
 //                    query-head rows ("columns") in the N dimension, D / 32
 //                    instructions chained in ascending d for Q.K and two
@@ -39,7 +39,7 @@ namespace vd {
 
 constexpr int kPage = 16;       // tokens per page
 constexpr int kTileKeys = 64;   // keys per online-softmax step
-constexpr int kSplitKeys = 512; // keys per split
+constexpr int kSplitKeys = 1024; // keys per split (256 and 2048 measured slower on decode)
 constexpr int kTilesPerSplit = kSplitKeys / kTileKeys;
 constexpr int kPagesPerTile = kTileKeys / kPage;
 constexpr int kSplitCols = 32;  // query-head rows per (request, KV head) on the split path

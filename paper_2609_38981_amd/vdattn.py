@@ -27,7 +27,7 @@ VD_OK = 0
 VD_ABI_VERSION = 4
 VD_DTYPE_BF16 = 1
 TILE_KEYS = 64
-SPLIT_KEYS = 512
+SPLIT_KEYS = 1024
 PAGE_SIZE = 16
 
 

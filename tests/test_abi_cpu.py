@@ -39,7 +39,7 @@ def test_create_supported_and_destroy(lib):
         assert rc == 0 and h.value
         a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
         assert lib.vd_attn_tiling(h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == 0
-        assert (a.value, b.value, c.value) == (64, 512, 16)
+        assert (a.value, b.value, c.value) == (64, 1024, 16)
         lib.vd_attn_destroy(h)
     lib.vd_attn_destroy(None)
 
@@ -65,8 +65,8 @@ def test_workspace_and_pool_sizes(lib):
     rc, h = _create(lib)
     n = ctypes.c_size_t()
     assert lib.vd_attn_workspace_size(h, 64, 1, 4096, ctypes.byref(n)) == 0
-    # m, z and U (D floats) per (request, KV head, 32 columns, 8 splits)
-    entries = 64 * 8 * 32 * 8
+    # m, z and U (D floats) per (request, KV head, 32 columns, 4 splits of 1024 keys)
+    entries = 64 * 8 * 32 * 4
     assert n.value >= entries * (2 + 128) * 4
     assert lib.vd_attn_workspace_size(h, -1, 1, 1, ctypes.byref(n)) == -1
     assert lib.vd_pool_bytes(h, 10, ctypes.byref(n)) == 0

@@ -77,7 +77,7 @@ def test_chunking_and_query_length(shape):
     U.assert_same_bits(whole, c512, min_common=n_total)
     U.assert_same_bits(whole, c128, min_common=n_total)
     # verify (s = 4) and decode (s = 1) steps around split and tile edges
-    spots = [1, 2, 63, 64, 65, 511, 512, 513, 1024, 1025, 1099]
+    spots = [1, 2, 63, 64, 65, 511, 512, 513, 1023, 1024, 1025, 1099]
     steps = [(p + 1, 1) for p in spots] + [(p + 1, 4) for p in spots if p >= 3]
     U.assert_same_bits(whole, run(steps), min_common=len(spots))
     # a batch that mixes all of them in one call

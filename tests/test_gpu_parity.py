@@ -85,13 +85,13 @@ def test_parity_small(name):
 
 
 EDGE_LENGTHS = [(1, 1), (2, 1), (16, 1), (17, 1), (63, 1), (64, 1), (65, 1), (511, 1), (512, 1),
-                (513, 1), (1024, 1), (1025, 1), (16, 16), (65, 9), (513, 8), (600, 120),
-                (1100, 1100)]
+                (513, 1), (1023, 1), (1024, 1), (1025, 1), (2047, 1), (2048, 1), (2049, 1),
+                (16, 16), (65, 9), (513, 8), (1025, 8), (600, 120), (1100, 1100)]
 
 
 @pytest.mark.parametrize("shape", [W.TINY, W.LLAMA8B, W.LLAMA70B], ids=["tiny", "8b", "70b"])
 def test_parity_edge_lengths(shape):
-    """Ragged tails around page (16), tile (64) and split (512) boundaries, on
+    """Ragged tails around page (16), tile (64) and split (1024) boundaries, on
     both the split path (few query rows) and the chunk path (many)."""
     prompts = [W.make_prompt(shape, n, 8, i, q_window=s) for i, (n, s) in enumerate(EDGE_LENGTHS)]
     reqs = [W.Req(i, n, s) for i, (n, s) in enumerate(EDGE_LENGTHS)]

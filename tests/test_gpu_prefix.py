@@ -1,6 +1,6 @@
 """GPU tests of the shared-prefix pass (calls with the shared_pages hint): the
 plan launch finds adjacent requests whose page tables start with the same
-pages, and the shared-prefix kernel computes their shared 512-key splits once
+pages, and the shared-prefix kernel computes their shared splits once
 for all their rows, storing the partial states the rows' own split items would
 have stored; the merge folds them with the rest.  Its output must be
 bit-identical to the same call without the pass (every split read by
@@ -11,6 +11,7 @@ from __future__ import annotations
 import numpy as np
 import pytest
 
+from paper_2609_38981_amd import vdattn as V
 from paper_2609_38981_amd import workloads as W
 from tests import gpu_util as U
 
@@ -23,38 +24,41 @@ def _gpu():
 
 
 def _groups_call(shape: W.Shape, shared: bool, cfg: int = 21) -> W.Call:
-    """Ten requests in groups of different depths.
+    """Ten requests in groups of different depths (S = the split size).
 
-    * 0..3 on a 1024-token prefix X (2 splits): verify, decode, a 120-row
+    * 0..3 on a 2S-token prefix X (2 splits): verify, decode, a 120-row
       prefill chunk (chunk path: in the group's range, not a member), decode;
     * 4: an unrelated decode (ends the group);
-    * 5, 6: two requests reading one 2000-token prompt Y, at n = 1800 and
-      n = 2000 (verify): they share 3 splits;
-    * 7..9 on X again, apart from 0..3: decode at n = 1424, decode at n = 1000
-      reading the same prompt as 7 (its row lies inside X's second split), and
-      a verify: they share 1 split.
+    * 5, 6: two requests reading one (4S - 48)-token prompt Y, at n = 3S + 300
+      and n = 4S - 48 (verify): they share 3 splits;
+    * 7..9 on X again, apart from 0..3: decode at n = 2S + 400, decode at
+      n = 2S - 24 reading the same prompt as 7 (its row lies inside X's second
+      split), and a verify: they share 1 split.
     ``shared``: the prompts on X share X's physical pages (else they hold
     copies)."""
-    X = W.make_prompt(shape, 1024, cfg, 90_000, q_window=0)
-    Y = W.make_prompt(shape, 2000, cfg, 90_001, q_window=256)
+    S = V.SPLIT_KEYS
+    X = W.make_prompt(shape, 2 * S, cfg, 90_000, q_window=0)
+    Y = W.make_prompt(shape, 4 * S - 48, cfg, 90_001, q_window=S)
     prompts = []
 
     def on_x(n, qw):
         prompts.append(W.make_prompt(shape, n, cfg, len(prompts), q_window=qw, prefix=X,
-                                     prefix_len=1024))
+                                     prefix_len=2 * S))
         return len(prompts) - 1
 
-    a0, a1, a2, a3 = on_x(1124, 4), on_x(1324, 1), on_x(1224, 120), on_x(1074, 1)
-    prompts.append(W.make_prompt(shape, 900, cfg, len(prompts), q_window=1))
+    a0, a1 = on_x(2 * S + 100, 4), on_x(2 * S + 300, 1)
+    a2, a3 = on_x(2 * S + 200, 120), on_x(2 * S + 50, 1)
+    prompts.append(W.make_prompt(shape, 2 * S - 124, cfg, len(prompts), q_window=1))
     z = len(prompts) - 1
     prompts.append(Y)
     y = len(prompts) - 1
-    a7, a9 = on_x(1424, 430), on_x(1084, 4)
-    reqs = [W.Req(a0, 1124, 4), W.Req(a1, 1324, 1), W.Req(a2, 1224, 120), W.Req(a3, 1074, 1),
-            W.Req(z, 900, 1), W.Req(y, 1800, 1), W.Req(y, 2000, 4),
-            W.Req(a7, 1424, 1), W.Req(a7, 1000, 1), W.Req(a9, 1084, 4)]
+    a7, a9 = on_x(2 * S + 400, 430), on_x(2 * S + 60, 4)
+    reqs = [W.Req(a0, 2 * S + 100, 4), W.Req(a1, 2 * S + 300, 1), W.Req(a2, 2 * S + 200, 120),
+            W.Req(a3, 2 * S + 50, 1), W.Req(z, 2 * S - 124, 1), W.Req(y, 3 * S + 300, 1),
+            W.Req(y, 4 * S - 48, 4), W.Req(a7, 2 * S + 400, 1), W.Req(a7, 2 * S - 24, 1),
+            W.Req(a9, 2 * S + 60, 4)]
     return W.place(shape, prompts, reqs, W.rng_for(cfg, 4 if shared else 5),
-                   shared_prefix_pages=64 if shared else 0)
+                   shared_prefix_pages=(2 * S) // shape.page_size if shared else 0)
 
 
 @pytest.mark.parametrize("shape", [W.LLAMA70B, W.Shape(16, 4, 64)], ids=["70b", "g4_d64"])
@@ -78,9 +82,9 @@ def test_prefix_groups(shape):
 
 
 def test_prefix_many_requests():
-    """300 requests on one 1024-token prefix (the plan launch lists the split
+    """300 requests on a prefix of one split (the plan launch lists the split
     items), and 1030 requests (more than the pass examines: it is off)."""
-    kw = dict(prefix=1024, suf_lo=20, suf_hi=120, shape=W.LLAMA8B)
+    kw = dict(prefix=V.SPLIT_KEYS, suf_lo=20, suf_hi=120, shape=W.LLAMA8B)
     big = W.config5(num_req=300, **kw)
     a_bits = U.gpu_run(big, shared_pages=True)
     a = U.by_position(big, a_bits)
@@ -102,7 +106,8 @@ def test_prefix_with_new_tokens():
     on; the same bits as without it and as with the tokens already in the
     pool."""
     for num_req in (12, 300):
-        call = W.config5(num_req=num_req, prefix=1024, suf_lo=30, suf_hi=200, shape=W.LLAMA8B)
+        call = W.config5(num_req=num_req, prefix=V.SPLIT_KEYS, suf_lo=30, suf_hi=200,
+                         shape=W.LLAMA8B)
         base = U.by_position(call, U.gpu_run(call, shared_pages=False))
         for sp in (True, False):
             U.assert_same_bits(base, U.by_position(call, U.gpu_run(call, append=True, shared_pages=sp)),
@@ -124,7 +129,8 @@ def test_prefix_lse():
 def test_prefix_deep():
     """A 36-split shared prefix: the pass covers its first 32 splits, the split
     items the rest, and the long merge (more than 16 splits) folds them all."""
-    call = W.config5(num_req=4, prefix=36 * 512, suf_lo=100, suf_hi=600, shape=W.LLAMA70B)
+    call = W.config5(num_req=4, prefix=36 * V.SPLIT_KEYS, suf_lo=100, suf_hi=600,
+                     shape=W.LLAMA70B)
     a_bits = U.gpu_run(call, shared_pages=True)
     a = U.by_position(call, a_bits)
     U.assert_same_bits(a, U.by_position(call, U.gpu_run(call, shared_pages=False)),

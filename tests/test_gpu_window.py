@@ -28,7 +28,7 @@ def outs(call, **kw):
     return U.by_position(call, U.gpu_run(call, **kw))
 
 
-# windows below a page, at and around the tile (64) and split (512) sizes
+# windows below a page, at and around the tile (64) and split (1024) sizes
 CASES = {
     "decode8b": lambda w: W.config2(batch=8, lo=100, hi=1800, shape=ws(W.LLAMA8B, w)),
     "mixed8b": lambda w: W.config3(num_prefill=2, chunk=96, max_off=1500, num_decode=6,
@@ -39,7 +39,8 @@ CASES = {
                                      [W.Req(0, 1300, 1300)], W.rng_for(9, 4)),
 }
 PARAMS = [(c, w) for c in sorted(CASES) for w in (1, 37, 64, 700)] + \
-    [("decode8b", 512), ("decode8b", 1500), ("mixed8b", 513), ("chunks_tiny", 200)]
+    [("decode8b", 512), ("decode8b", 1024), ("decode8b", 1500), ("mixed8b", 513),
+     ("mixed8b", 1025), ("chunks_tiny", 200)]
 
 
 @pytest.mark.parametrize("case,w", PARAMS, ids=["%s-w%d" % p for p in PARAMS])
@@ -113,7 +114,7 @@ def test_window_chunking_and_query_length(shape):
     c128 = run([(min(n_total, e + 128), min(128, n_total - e)) for e in range(0, n_total, 128)])
     U.assert_same_bits(whole, c512, min_common=n_total)
     U.assert_same_bits(whole, c128, min_common=n_total)
-    spots = [1, 63, 64, 65, 299, 300, 301, 511, 512, 513, 700, 1024, 1025, 1099]
+    spots = [1, 63, 64, 65, 299, 300, 301, 511, 512, 513, 700, 1023, 1024, 1025, 1099]
     steps = [(p + 1, 1) for p in spots] + [(p + 1, 4) for p in spots if p >= 3]
     U.assert_same_bits(whole, run(steps), min_common=len(spots))
     reqs = [W.Req(0, n, s) for n, s in [(1100, 600), (513, 1), (700, 4), (65, 65), (1025, 8)]]
