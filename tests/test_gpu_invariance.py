@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 import torch
 
+from paper_2609_38981_amd import vdattn as V
 from paper_2609_38981_amd import workloads as W
 from tests import gpu_util as U
 
@@ -175,6 +176,18 @@ def test_large_batch_plan_launch():
     U.assert_same_bits(small, outs(large, append=True), min_common=3 * 96 + 10)
     U.assert_same_bits(small, outs(W.config3(num_decode=10, **kw3), append=True),
                        min_common=3 * 96 + 10)
+
+
+def test_large_batch_column_halves():
+    """More than 256 requests with 32 query-head rows per KV head (70B verify,
+    s = 4): the plan launch lists two column-half items per split.  Rows equal
+    those of a few of the requests run alone (the split workgroups' own
+    planning), and those without the shared-prefix pass."""
+    big = W.config5(num_req=300, prefix=V.SPLIT_KEYS, suf_lo=20, suf_hi=300)
+    a = outs(big)
+    U.assert_same_bits(a, outs(big.subcall([0, 1, 150, 298, 299])), min_common=4 * 3 + 2)
+    U.assert_same_bits(a, outs(big, shared_pages=False), min_common=big.total_q_tokens)
+    U.say("  300 verify requests: %s" % U.parity(big, U.gpu_run(big), rows=[0, 3, 601, 749]))
 
 
 def test_long_context_batch_and_placement():

@@ -71,6 +71,11 @@ SMALL = {
     "cfg5_verify_small": lambda: W.config5(num_req=6, prefix=256, suf_lo=20, suf_hi=80),
     "d64_prefill_chunks": lambda: W.place(W.TINY, [W.make_prompt(W.TINY, 700, 9, 0)],
                                           [W.Req(0, 700, 700)], W.rng_for(9, 4)),
+    # 32 query heads per KV head: a one-row decode has 32 query-head rows, two
+    # split items per split (column halves)
+    "g32_decode": lambda: W.config2(batch=6, lo=100, hi=2500, shape=W.Shape(32, 1, 128), cfg=7),
+    "g32_d64_mixed": lambda: W.config3(num_prefill=1, chunk=20, max_off=900, num_decode=5,
+                                       dec_lo=50, dec_hi=2200, shape=W.Shape(64, 2, 64), cfg=7),
 }
 
 
