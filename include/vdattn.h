@@ -208,6 +208,22 @@ int vd_attn_forward_chunks_timed(const vd_attn* h, const vd_attn_batch* batch, v
                                  const void* workspace, size_t workspace_bytes,
                                  hipStream_t stream, hipEvent_t start, hipEvent_t stop);
 
+/* Opt-in check of the batch's device-side data, the preconditions the host cannot see
+ * (Appendix A.1: 0 < s_r <= n_r; page ids within the pool).  One kernel on `stream`; reads
+ * only.  status: device int32 [num_seqs]; status[r] receives the bit mask of what request r
+ * violates (0: nothing):
+ *    1  s_r < 1 or s_r > n_r (cu_q_lens, context_lens);
+ *    2  s_r > max_q_len or n_r > max_context_len (the host hints);
+ *    4  ceil(n_r / 16) > pt_stride;
+ *    8  cu_q_lens[r] < 0 or cu_q_lens[r + 1] > total_q_tokens;
+ *   16  a page id among the entries 0 .. ceil(n_r / 16) - 1 of its table row (those
+ *       within the stride) lies outside [0, num_pages).
+ * vd_attn_forward skips a request with any of bits 1, 2, 4, 8 (its output rows are left
+ * unwritten) and reads a page with bit 16's ids as zeros.  Host-visible errors as for
+ * vd_attn_forward; a batch with no request returns VD_OK without a launch. */
+int vd_attn_validate(const vd_attn* h, const vd_attn_batch* batch, int32_t* status,
+                     hipStream_t stream);
+
 /* Bytes of ONE pool (K or V) holding num_pages pages. */
 int vd_pool_bytes(const vd_attn* h, int64_t num_pages, size_t* bytes);
 

@@ -1857,6 +1857,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }
 
 // ---------------------------------------------------------------------------
+// Opt-in check of a batch's device-side data: one wavefront per request
+// writes the bit mask of the preconditions the request violates (the
+// status codes of vd_attn_validate).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void validate_kernel(const int32_t* cu, const int32_t* ctx,
+                                                      const int32_t* pt, int32_t pt_stride,
+                                                      int64_t num_pages, int64_t T, int32_t max_q,
+                                                      int32_t max_ctx, int32_t num_seqs,
+                                                      int32_t* status) {
+  const int r = blockIdx.x;
+  if (r >= num_seqs) return;
+  const int lane = __lane_id();
+  const int q0 = cu[r], q1 = cu[r + 1], n = ctx[r];
+  const int64_t s = (int64_t)q1 - q0;
+  int st = 0;
+  if (s < 1 || s > n) st |= 1;
+  if (s > max_q || n > max_ctx) st |= 2;
+  const int64_t npages = n > 0 ? ((int64_t)n + kPage - 1) / kPage : 0;
+  if (npages > pt_stride) st |= 4;
+  if (q0 < 0 || (int64_t)q1 > T) st |= 8;
+  // page ids of the table entries the request reads (within its row)
+  const int ne = (int)(npages < pt_stride ? npages : pt_stride);
+  bool bad = false;
+  for (int e = lane; e < ne; e += 64) {
+    const int32_t pg = pt[(int64_t)r * pt_stride + e];
+    bad = bad || pg < 0 || pg >= num_pages;
+  }
+  if (__any(bad)) st |= 16;
+  if (lane == 0) status[r] = st;
+}
+
+// ---------------------------------------------------------------------------
 // KV write: one thread per (token, KV head, 8 consecutive d)
 template <int D>
 __global__ __launch_bounds__(256) void kv_write_kernel(const uint16_t* knew, const uint16_t* vnew,
@@ -2263,6 +2295,18 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* b, void* out, void* w
   rc = vd_attn_forward_chunks(h, b, out, workspace, workspace_bytes, stream);
   if (rc != VD_OK) return rc;
   return vd_attn_forward_merge(h, b, out, workspace, workspace_bytes, stream);
+}
+
+int vd_attn_validate(const vd_attn* h, const vd_attn_batch* b, int32_t* status,
+                     hipStream_t stream) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK || b->num_seqs == 0) return rc;
+  if (!status || !b->cu_q_lens || !b->context_lens || !b->page_table || b->pt_stride < 1)
+    return VD_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)b->num_seqs), dim3(64), 0, stream,
+                     b->cu_q_lens, b->context_lens, b->page_table, b->pt_stride, b->num_pages,
+                     b->total_q_tokens, b->max_q_len, b->max_context_len, b->num_seqs, status);
+  return launched();
 }
 
 int vd_pool_bytes(const vd_attn* h, int64_t num_pages, size_t* bytes) {

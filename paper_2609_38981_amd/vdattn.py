@@ -82,6 +82,7 @@ def load_library(path: str = LIB_PATH):
         "vd_attn_forward_chunks_timed": (ctypes.c_int,
                                          [P, ctypes.POINTER(_Batch), P, P, SZ, P, P, P]),
         "vd_pool_bytes": (ctypes.c_int, [P, I64, ctypes.POINTER(SZ)]),
+        "vd_attn_validate": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P]),
         "vd_kv_write": (ctypes.c_int, [P, P, P, P, I64, P, P, I64, P]),
         "vd_linear": (ctypes.c_int, [P, I64, P, I64, P, I64, I64, I32, I32, P]),
         "vd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -294,6 +295,15 @@ class VdAttn:
         """Marshals one call's arguments once, for callers that launch the same
         call (same tensors, same stream) many times."""
         return PreparedCall(self, b, out, workspace, stream)
+
+    def validate(self, b: Batch, stream=None) -> torch.Tensor:
+        """Per-request bit masks of the device-side preconditions each request
+        violates (0: none), as int32 [num_seqs] on the device; see vd_attn_validate."""
+        cb = self._batch(b)
+        status = torch.full((int(b.context_lens.numel()),), -1, dtype=torch.int32, device="cuda")
+        _check(self.lib.vd_attn_validate(self._h, ctypes.byref(cb), _ptr(status), _stream(stream)),
+               "vd_attn_validate")
+        return status
 
     def kv_write(self, k_new: torch.Tensor, v_new: torch.Tensor, slot_mapping: torch.Tensor,
                  k_pool: torch.Tensor, v_pool: torch.Tensor, num_pages: int, stream=None):
