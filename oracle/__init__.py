@@ -61,6 +61,11 @@ def bind(path: str):
         ctypes.c_int, ctypes.c_double, ctypes.c_int, P, P, P, P, ctypes.c_int, P, P,
         ctypes.c_int64, P, P, P, ctypes.c_int]
     lib.vdo_default_threads.restype = ctypes.c_int
+    if hasattr(lib, "vdo_dense_attention"):
+        lib.vdo_dense_attention.restype = ctypes.c_int
+        lib.vdo_dense_attention.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                            ctypes.c_int, ctypes.c_double, ctypes.c_int, P, P, P,
+                                            P, P]
     if hasattr(lib, "vdo_linear"):
         lib.vdo_linear.restype = ctypes.c_int
         lib.vdo_linear.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.c_int, P, ctypes.c_int64,
@@ -142,6 +147,33 @@ def paged_attention(q_bits, cu_q_lens, context_lens, page_table, k_pool_bits, v_
         cup, ctxp, ptp, stride, kpp, vpp, kp.shape[0], selp,
         out.ctypes.data_as(ctypes.c_void_p),
         lse.ctypes.data_as(ctypes.c_void_p) if with_lse else None, int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the call: %s (%d)" % (ERRORS.get(rc, "?"), rc))
+    return (out, lse) if with_lse else out
+
+
+def dense_attention(q_bits, k_bits, v_bits, *, num_q_heads, num_kv_heads, head_dim, scale=None,
+                    window=0, lib=None, with_lse=False):
+    """Exact (fp64) causal attention of one request whose keys and values are
+    contiguous (no page table): the dense variant of ``paged_attention``.
+
+    q_bits: uint16 [s, Hq, D]; k_bits, v_bits: uint16 [n, Hkv, D] (bf16 bit
+    patterns); row i stands for position n - s + i.  Returns float64
+    [s, Hq, D] (and the log-sum-exp [s, Hq] with ``with_lse``)."""
+    lib = _load() if lib is None else lib
+    q, qp = _c(q_bits, np.uint16)
+    k, kp = _c(k_bits, np.uint16)
+    v, vp = _c(v_bits, np.uint16)
+    s, n = q.shape[0], k.shape[0]
+    assert q.shape == (s, num_q_heads, head_dim), q.shape
+    assert k.shape == v.shape == (n, num_kv_heads, head_dim), (k.shape, v.shape)
+    if scale is None:
+        scale = 1.0 / np.sqrt(head_dim)
+    out = np.full((s, num_q_heads, head_dim), np.nan, np.float64)
+    lse = np.full((s, num_q_heads), np.nan, np.float64) if with_lse else None
+    rc = lib.vdo_dense_attention(s, n, num_q_heads, num_kv_heads, head_dim, float(scale),
+                                 int(window), qp, kp, vp, out.ctypes.data_as(ctypes.c_void_p),
+                                 lse.ctypes.data_as(ctypes.c_void_p) if with_lse else None)
     if rc != 0:
         raise ValueError("oracle rejected the call: %s (%d)" % (ERRORS.get(rc, "?"), rc))
     return (out, lse) if with_lse else out

@@ -246,6 +246,65 @@ int vdo_paged_attention(int num_seqs, int64_t total_q_tokens, int num_q_heads,
   return failed ? VDO_ERR_NOMEM : VDO_OK;
 }
 
+/* The same attention for one request whose keys and values are contiguous,
+ * with no page table: q [s][hq][d], k and v [n][hkv][d] (bf16 bits); row i
+ * is position p = n - s + i; out [s][hq][d] in double, lse [s][hq] optional
+ * (NULL: not written).  Single-threaded; the definition written out again,
+ * so that the page-table gather of vdo_paged_attention can be checked
+ * against it. */
+int vdo_dense_attention(int s, int n, int num_q_heads, int num_kv_heads,
+                        int head_dim, double scale, int window,
+                        const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                        double *out, double *lse) {
+  if (!q || !k || !v || !out) return VDO_ERR_ARG;
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 ||
+      num_q_heads % num_kv_heads != 0 || window < 0)
+    return VDO_ERR_ARG;
+  if (s < 1 || s > n) return VDO_ERR_LENGTHS;
+  const int hq = num_q_heads, hkv = num_kv_heads, D = head_dim;
+  double *score = (double *)malloc(sizeof(double) * (size_t)n);
+  double *w = (double *)malloc(sizeof(double) * (size_t)n);
+  if (!score || !w) {
+    free(score);
+    free(w);
+    return VDO_ERR_NOMEM;
+  }
+  for (int i = 0; i < s; ++i) {
+    const int p = i + (n - s); /* position of row i */
+    const int lo = (window > 0 && p - window + 1 > 0) ? p - window + 1 : 0;
+    for (int h = 0; h < hq; ++h) {
+      const int g = h / (hq / hkv);
+      const uint16_t *qrow = q + ((int64_t)i * hq + h) * D;
+      for (int j = lo; j <= p; ++j) {
+        const uint16_t *krow = k + ((int64_t)j * hkv + g) * D;
+        double acc = 0.0;
+        for (int dd = 0; dd < D; ++dd)
+          acc += bf16_to_double(qrow[dd]) * bf16_to_double(krow[dd]);
+        score[j] = scale * acc;
+      }
+      double mx = -INFINITY;
+      for (int j = lo; j <= p; ++j)
+        if (score[j] > mx) mx = score[j];
+      double denom = 0.0;
+      for (int j = lo; j <= p; ++j) {
+        w[j] = exp(score[j] - mx);
+        denom += w[j];
+      }
+      for (int j = lo; j <= p; ++j) w[j] = w[j] / denom;
+      if (lse) lse[(int64_t)i * hq + h] = mx + log(denom);
+      double *orow = out + ((int64_t)i * hq + h) * D;
+      for (int dd = 0; dd < D; ++dd) orow[dd] = 0.0;
+      for (int j = lo; j <= p; ++j) {
+        const uint16_t *vrow = v + ((int64_t)j * hkv + g) * D;
+        for (int dd = 0; dd < D; ++dd) orow[dd] += w[j] * bf16_to_double(vrow[dd]);
+      }
+    }
+  }
+  free(score);
+  free(w);
+  return VDO_OK;
+}
+
 /* Number of host threads the oracle uses when asked for "all cores". */
 int vdo_default_threads(void) { return (int)sysconf(_SC_NPROCESSORS_ONLN); }
 

@@ -122,8 +122,13 @@ def parity(call: W.Call, gpu_bits: np.ndarray, rows=None) -> dict:
         ref = oracle_run(sub, sub_rows)[sub_rows]
     diff = np.abs(got[sel] - ref)
     assert np.isfinite(got[sel]).all(), "non-finite GPU output"
+    # the error in units of the bf16 spacing at the reference value (8 significant
+    # bits: 2^(e - 7) for |ref| in [2^e, 2^(e+1)), down to the smallest normal)
+    e = np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -126)))
+    ulps = diff / np.exp2(e - 7)
     st = dict(max_abs=float(diff.max()) if diff.size else 0.0,
-              mean_abs=float(diff.mean()) if diff.size else 0.0, rows=int(len(sel)))
+              mean_abs=float(diff.mean()) if diff.size else 0.0,
+              max_bf16_ulp=float(ulps.max()) if ulps.size else 0.0, rows=int(len(sel)))
     assert st["max_abs"] <= TOL, st
     return st
 

@@ -259,6 +259,30 @@ def pin_invariances(lib):
             assert np.array_equal(val, base[key]), key
 
 
+def pin_paged_equals_dense(lib):
+    """The page-table gather: every request of a paged call (random page
+    placement in a NaN-poisoned pool, several requests, GQA, a window) gives
+    exactly the bits of the same request over contiguous keys and values (the
+    dense variant, written separately with no page table)."""
+    rng = np.random.default_rng(41)
+    hq, hkv, d, P = 6, 2, 32, 16
+    reqs = [rand_req(rng, s, n, hq, hkv, d) for s, n in [(1, 1), (3, 17), (1, 64), (5, 70),
+                                                       (16, 33), (2, 130)]]
+    for window in (0, 20):
+        for scale in (None, 0.3):
+            out, lse = run(lib, reqs, hq, hkv, d, P, scale=scale, window=window, with_lse=True,
+                           rng=np.random.default_rng(window + 7))
+            t = 0
+            for r in reqs:
+                s = r["q"].shape[0]
+                dense, dlse = oracle.dense_attention(r["q"], r["k"], r["v"], num_q_heads=hq,
+                                                     num_kv_heads=hkv, head_dim=d, scale=scale,
+                                                     window=window, lib=lib, with_lse=True)
+                assert np.array_equal(out[t:t + s], dense), (s, window, scale)
+                assert np.array_equal(lse[t:t + s], dlse), (s, window, scale)
+                t += s
+
+
 # -- sliding window (Appendix A.5: key j visible to p when p - w < j <= p) ----
 def pin_sdpa_window(lib):
     """Chunks at key offsets with a sliding window equal SDPA with a banded
@@ -443,7 +467,8 @@ def pin_linear_fsum_bound(lib):
             assert abs(c[m, n] - math.fsum(prods)) <= bound, (m, n)
 
 
-ALL_PINS = [pin_sdpa_prefill, pin_sdpa_chunk_offset, pin_sdpa_scale, pin_scipy_softmax_dense,
+ALL_PINS = [pin_paged_equals_dense, pin_sdpa_prefill, pin_sdpa_chunk_offset, pin_sdpa_scale,
+            pin_scipy_softmax_dense,
             pin_single_key, pin_zero_query_mean, pin_identical_keys_mean, pin_dominant_key,
             pin_fig4_example, pin_invariances, pin_sdpa_window, pin_window_one_key,
             pin_window_zero_query_mean, pin_window_limits, pin_lse_scipy, pin_lse_closed_forms,
