@@ -105,10 +105,34 @@ def host_threads() -> int:
     return max(n, 1)
 
 
-def cpu_baseline(call, min_seconds: float = 10.0, max_requests: int = 64):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def err_vs_gpu(got, ref) -> dict:
+    """The GPU output against the oracle: the largest absolute difference, and
+    the largest in units of the bf16 spacing at the oracle value (8 significant
+    bits: 2^(e - 7) for |ref| in [2^e, 2^(e+1)), down to the smallest normal);
+    the output's own bf16 rounding alone accounts for up to half a unit."""
+    diff = np.abs(got - ref)
+    e = np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -126)))
+    return {"max_abs_err_vs_gpu": float(diff.max()),
+            "max_bf16_ulp_vs_gpu": round(float((diff / np.exp2(e - 7)).max()), 3)}
+
+
+def cpu_baseline(call, gpu_bits=None, min_seconds: float = 10.0, max_requests: int = 64):
     """The oracle on the host on a bounded sample of the same workload: the
     first requests of the batch (whole requests), repeated until at least
-    ``min_seconds`` of wall time.  Returns KV GB/s of the sample."""
+    ``min_seconds`` of wall time.  Returns KV GB/s of the sample and, with the
+    GPU output of the whole call (``gpu_bits``, uint16 [T, Hq, D]), the largest
+    difference between the oracle and the GPU on the sample's rows."""
     import oracle
     from paper_2609_38981_amd import workloads as W
 
@@ -130,17 +154,22 @@ def cpu_baseline(call, min_seconds: float = 10.0, max_requests: int = 64):
     threads = host_threads()
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.paged_attention(*args, threads=threads, **kw)
+        ref = oracle.paged_attention(*args, threads=threads, **kw)
         reps += 1
         el = time.perf_counter() - t0
         if el >= min_seconds or reps >= 1000:
             break
     sec = el / reps
-    return {"value": round(sub.kv_bytes() / sec / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle",
-            "sample": "%d of %d requests (%d query rows, %.1f MB K+V), %d repetitions, %.2f s "
-                      "per repetition" % (len(reqs), call.num_seqs, sub.total_q_tokens,
-                                          sub.kv_bytes() / 1e6, reps, sec)}
+    res = {"value": round(sub.kv_bytes() / sec / 1e9, 4), "unit": "GB/s", "cores": threads,
+           "kind": "oracle", "cpu_model": cpu_model(),
+           "sample": "%d of %d requests (%d query rows, %.1f MB K+V), %d repetitions, %.2f s "
+                     "per repetition" % (len(reqs), call.num_seqs, sub.total_q_tokens,
+                                         sub.kv_bytes() / 1e6, reps, sec)}
+    if gpu_bits is not None:
+        # the sample's rows are the call's first rows
+        got = W.bf16_to_f32(gpu_bits[:sub.total_q_tokens]).astype(np.float64)
+        res.update(err_vs_gpu(got, ref))
+    return res
 
 
 # The batch-invariant linear layer (vd_linear): (M tokens, N outputs, K inputs)
@@ -151,9 +180,13 @@ LINEAR_WORKLOADS = {
 }
 
 
-def linear_cpu_baseline(a_bits, b_bits, min_seconds: float = 10.0):
+def linear_cpu_baseline(a_bits, b_bits, gpu_bits=None, min_seconds: float = 10.0):
     """The oracle (fp64 plain loops) on a bounded sample of the same layer: the
-    first rows of the activations, repeated until at least ``min_seconds``."""
+    first rows of the activations, repeated until at least ``min_seconds``;
+    with the GPU output (``gpu_bits``, uint16 [M, N]), the largest absolute
+    difference from the oracle on the sample's rows."""
+    from paper_2609_38981_amd import workloads as W
+
     import oracle
 
     M, K = a_bits.shape
@@ -162,16 +195,20 @@ def linear_cpu_baseline(a_bits, b_bits, min_seconds: float = 10.0):
     threads = host_threads()
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.linear(a_bits[:rows], b_bits, threads=threads)
+        ref = oracle.linear(a_bits[:rows], b_bits, threads=threads)
         reps += 1
         el = time.perf_counter() - t0
         if el >= min_seconds or reps >= 1000:
             break
     sec = el / reps
-    return {"value": round(2.0 * rows * N * K / sec / 1e12, 6), "unit": "TFLOP/s",
-            "cores": threads, "kind": "oracle",
-            "sample": "%d of %d rows (%d x %d x %d), %d repetitions, %.2f s per repetition"
-                      % (rows, M, rows, N, K, reps, sec)}
+    res = {"value": round(2.0 * rows * N * K / sec / 1e12, 6), "unit": "TFLOP/s",
+           "cores": threads, "kind": "oracle", "cpu_model": cpu_model(),
+           "sample": "%d of %d rows (%d x %d x %d), %d repetitions, %.2f s per repetition"
+                     % (rows, M, rows, N, K, reps, sec)}
+    if gpu_bits is not None:
+        got = W.bf16_to_f32(gpu_bits[:rows]).astype(np.float64)
+        res.update(err_vs_gpu(got, ref))
+    return res
 
 
 def bench_linear(args):
@@ -204,6 +241,7 @@ def bench_linear(args):
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
     k_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    gpu_bits = S.bits_of(reps[0][2])  # before torch.matmul below overwrites it
     flop = 2.0 * M * N * K
     ach = flop / (k_ms * 1e-3) / 1e12
     # context: the vendor library GEMM on the same shapes (not batch-invariant in general)
@@ -238,7 +276,7 @@ def bench_linear(args):
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        res["cpu_baseline"] = linear_cpu_baseline(a_bits, b_bits)
+        res["cpu_baseline"] = linear_cpu_baseline(a_bits, b_bits, gpu_bits)
     print(json.dumps(res), flush=True)
 
 
@@ -428,9 +466,26 @@ def main():
                                 zip(["plan_and_kv_write", "splits", "chunks", "merge"], ph_ms)},
         "roofline": roof,
     }
+    # outside the timed region: the output of the timed call, and the first and
+    # last requests run alone, whose rows must be bit-identical to the batched ones
+    gpu_bits = S.bits_of(reps[0][2])
+    probe = sorted({0, call.num_seqs - 1})
+    alone = call.subcall(probe)
+    dca = S.to_device(attn, alone, poison=False)
+    wsa = attn.new_workspace(alone.num_seqs, dca.batch.max_q_len, dca.batch.max_context_len)
+    outa = torch.empty_like(dca.batch.q)
+    attn.forward(dca.batch, out=outa, workspace=wsa)
+    torch.cuda.synchronize()
+    bits_a = S.bits_of(outa)
+    same = 0
+    for k, ri in enumerate(probe):
+        for p in call.reqs[ri].positions:
+            same += int(np.array_equal(bits_a[alone.row_of(k, p)], gpu_bits[call.row_of(ri, p)]))
+    res["invariance"] = {"rows": int(alone.total_q_tokens), "bit_identical": same,
+                         "variant": "requests %s alone vs in the timed batch" % probe}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        res["cpu_baseline"] = cpu_baseline(call)
+        res["cpu_baseline"] = cpu_baseline(call, gpu_bits)
     print(json.dumps(res), flush=True)
 
 
