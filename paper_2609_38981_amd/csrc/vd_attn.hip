@@ -1434,6 +1434,27 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
 #endif
 constexpr int kChunkStages = VD_CHUNK_STAGES;
 
+// Entries lp0 .. lp0 + NE - 1 of a page-table row into spid (every thread of
+// a 256-thread workgroup takes part; the caller synchronises): the page id,
+// or -1 for an entry at or past npages or outside the pool.  Only entries
+// below npages are read.  The shared-prefix kernel stages a split's page ids
+// this way, so that a tile's page lookups are LDS reads, not dependent scalar
+// loads between the tile's barrier and its copies.
+template <int NE>
+__device__ __forceinline__ void load_pid_window(const Params& P, const int32_t* ptrow, int lp0,
+                                                int npages, int32_t* spid) {
+  static_assert(NE % 256 == 0 || NE < 256, "window size");
+#pragma unroll
+  for (int e0 = 0; e0 < NE; e0 += 256) {
+    const int e = e0 + (int)threadIdx.x;
+    if (NE >= 256 || e < NE) {
+      const int lp = lp0 + e;
+      int page = lp < npages ? ptrow[lp] : -1;
+      spid[e] = (page < 0 || page >= P.num_pages) ? -1 : page;
+    }
+  }
+}
+
 // Two workgroups per CU (waves_per_eu 2: at most 256 registers per lane, and
 // two LDS rings of kChunkStages tiles): while one wavefront of a SIMD waits on
 // its softmax chain, the other issues matrix-core work.  WIN: the handle has a
@@ -1612,10 +1633,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
       for (int m = 0; m < D / 16; ++m) {
         const int o = 256 * m + 4 * lane;
-        const u16x8 v0 = cat4(*reinterpret_cast<const u16x4*>(T + 4 * BLK + o),
-                              *reinterpret_cast<const u16x4*>(T + 5 * BLK + o));
-        const u16x8 v1 = cat4(*reinterpret_cast<const u16x4*>(T + 6 * BLK + o),
-                              *reinterpret_cast<const u16x4*>(T + 7 * BLK + o));
+        const u16x8 v0 = cat4(lds_read8<u16x4>(T + 4 * BLK + o), lds_read8<u16x4>(T + 5 * BLK + o));
+        const u16x8 v1 = cat4(lds_read8<u16x4>(T + 6 * BLK + o), lds_read8<u16x4>(T + 7 * BLK + o));
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) tile_pv_block<D>(st[nb], w[nb], m, v0, v1);
       }
@@ -1659,6 +1678,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 template <int D>
 constexpr size_t chunk_lds_bytes() {
   return (size_t)kChunkStages * 2 * kPagesPerTile * kPage * D * sizeof(uint16_t);
+}
+
+// ... and of the shared-prefix kernel: the same ring, then the page ids of an
+// item's split.
+template <int D>
+constexpr size_t prefix_lds_bytes() {
+  return chunk_lds_bytes<D>() + (size_t)(kSplitKeys / kPage) * sizeof(int32_t);
 }
 
 // ---------------------------------------------------------------------------
@@ -1705,6 +1731,13 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
   const int r0 = first + find_req(P.cu + first, end - first, t0 + c0 / P.G);
   const int nr = min(end - r0, kChunkCols);  // the rows reach requests r0 .. r0 + nr - 1
   if ((int)threadIdx.x <= nr) scu[threadIdx.x] = P.cu[r0 + threadIdx.x];
+  const int32_t* ptrow = P.pt + (int64_t)first * P.pt_stride;
+  // 1024 cg <= nh: every shared page is in the first member's table row
+  const int nh = (int)min<int64_t>(P.ctx[first], (int64_t)P.pt_stride * kPage);
+  const int kt0 = k * kTilesPerSplit, ntiles = kTilesPerSplit;
+  // the split's page ids (kSplitKeys / kPage entries from kt0's first) in LDS
+  int32_t* spid = reinterpret_cast<int32_t*>(lds + STAGES * TILE);
+  load_pid_window<kSplitKeys / kPage>(P, ptrow, kt0 * kPagesPerTile, (nh + kPage - 1) / kPage, spid);
   __syncthreads();
 
   bool live[NB];
@@ -1737,20 +1770,19 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
   }
   const bool wave_live = __any(live[0] || live[1]);
 
-  const int32_t* ptrow = P.pt + (int64_t)first * P.pt_stride;
-  // 1024 cg <= nh: every shared page is in the first member's table row
-  const int nh = (int)min<int64_t>(P.ctx[first], (int64_t)P.pt_stride * kPage);
-  const int kt0 = k * kTilesPerSplit, ntiles = kTilesPerSplit;
+  // the page ids of tile kt (-1: no page), one broadcast LDS read
+  auto tile_pages = [&](int kt) {
+    return *reinterpret_cast<const int4*>(spid + (kt - kt0) * kPagesPerTile);
+  };
   auto fetch = [&](int kt, int buf) {
-    int64_t pb[kPagesPerTile];
-#pragma unroll
-    for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt * kPagesPerTile + b, nh, g);
+    const int4 pg = tile_pages(kt);
+    const int pages[kPagesPerTile] = {pg.x, pg.y, pg.z, pg.w};
 #pragma unroll
     for (int w = 0; w < WCH; ++w) {
       const int q = wave * WCH + w;
       const int blk = q / (BLK / 512), sub = q % (BLK / 512);
-      const int b = blk % kPagesPerTile;
-      const int64_t pbb = pb[b] < 0 ? 0 : pb[b];
+      const int page = uni(pages[blk % kPagesPerTile]);
+      const int64_t pbb = page < 0 ? 0 : (int64_t)page * P.hkv + g;
       const uint16_t* src =
           block_ptr<D>(blk < kPagesPerTile ? P.kpool : P.vpool, pbb) + 512 * sub + 8 * lane;
       const uint32_t dst = (uint32_t)(uintptr_t)(lds + (buf * NBLK + blk) * BLK + 512 * sub);
@@ -1759,17 +1791,12 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
   };
   // a page id outside the pool reads as zeros, as on the split path
   auto pages_ok = [&](int kt) {
-    bool ok = true;
-#pragma unroll
-    for (int b = 0; b < kPagesPerTile; ++b)
-      ok = ok && page_block(P, ptrow, kt * kPagesPerTile + b, nh, g) >= 0;
-    return ok;
+    const int4 pg = tile_pages(kt);
+    return min(min(pg.x, pg.y), min(pg.z, pg.w)) >= 0;
   };
   auto zero_pages = [&](int kt, int buf) {
-    bool pvalid[kPagesPerTile];
-#pragma unroll
-    for (int b = 0; b < kPagesPerTile; ++b)
-      pvalid[b] = page_block(P, ptrow, kt * kPagesPerTile + b, nh, g) >= 0;
+    const int4 pg = tile_pages(kt);
+    const bool pvalid[kPagesPerTile] = {pg.x >= 0, pg.y >= 0, pg.z >= 0, pg.w >= 0};
     for (int ch = threadIdx.x; ch < TILE / 8; ch += 256) {
       const int blk = ch / (BLK / 8);
       if (!pvalid[blk % kPagesPerTile])
@@ -1812,10 +1839,8 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
 #pragma unroll
       for (int m = 0; m < D / 16; ++m) {
         const int o = 256 * m + 4 * lane;
-        const u16x8 v0 = cat4(*reinterpret_cast<const u16x4*>(T + 4 * BLK + o),
-                              *reinterpret_cast<const u16x4*>(T + 5 * BLK + o));
-        const u16x8 v1 = cat4(*reinterpret_cast<const u16x4*>(T + 6 * BLK + o),
-                              *reinterpret_cast<const u16x4*>(T + 7 * BLK + o));
+        const u16x8 v0 = cat4(lds_read8<u16x4>(T + 4 * BLK + o), lds_read8<u16x4>(T + 5 * BLK + o));
+        const u16x8 v1 = cat4(lds_read8<u16x4>(T + 6 * BLK + o), lds_read8<u16x4>(T + 7 * BLK + o));
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) tile_pv_block<D>(st[nb], w[nb], m, v0, v1);
       }
@@ -1842,7 +1867,8 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
 // workgroups run in turn: the grid is sized to the chip, not to the list.
 template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefix_kernel(Params P) {
-  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];  // [STAGES][8 page blocks]
+  // [STAGES][8 page blocks], then the page ids of an item's split
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   __shared__ int scu[kChunkCols + 1];  // cu of the requests an item's rows may belong to
   const int ngroups = P.casc_hdr[0], per_head = P.casc_hdr[1];
   if (ngroups < 1 || ngroups > P.num_seqs / 2 || per_head < 1 || per_head > (1 << 24)) return;
@@ -2088,7 +2114,7 @@ int run_prefix(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr) {
                         ((P.T * P.G + kChunkCols - 1) / kChunkCols + P.num_seqs / 2) *
                         std::min(kCascMaxSplits, std::max(P.max_splits - 1, 1));
   const int64_t blocks = (std::min<int64_t>(bound, 2 * 256) + 7) / 8 * 8;
-  constexpr size_t lds = chunk_lds_bytes<D>();
+  constexpr size_t lds = prefix_lds_bytes<D>();
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(&prefix_kernel<D>), hipFuncAttributeMaxDynamicSharedMemorySize,
       (int)lds);

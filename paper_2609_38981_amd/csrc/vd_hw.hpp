@@ -34,6 +34,17 @@ __device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0val) {
       : "memory");
 }
 
+// 8-byte LDS read issued as its own ds_read_b64.  Volatile, so that the
+// compiler does not pair it with a neighbour at another offset into one
+// two-address read: the two halves of a matrix operand come from two page
+// blocks, and a paired read would land them in the wrong registers and cost
+// register copies.
+template <class T8>
+__device__ __forceinline__ T8 lds_read8(const void* p) {
+  static_assert(sizeof(T8) == 8, "8-byte value");
+  return *(const volatile __attribute__((address_space(3))) T8*)(uintptr_t)p;
+}
+
 // Workgroup barrier that orders LDS accesses only (global memory operations
 // in flight are not waited for).
 __device__ __forceinline__ void lds_barrier() {
