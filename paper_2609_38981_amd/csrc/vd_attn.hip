@@ -1613,9 +1613,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const uint16_t* T = lds + buf * NBLK * BLK;
     if (wave_pmax >= j0 && j0 + kTileKeys - 1 >= wave_lo) {
       f32x4 acc[NB][kPagesPerTile];
+      // The two wavefronts of a SIMD belong to different workgroups; the one
+      // issuing matrix-core work gets the higher issue priority, the other's
+      // softmax fills the vector ALU around it.
+      __builtin_amdgcn_s_setprio(2);
       tile_scores<D, NB>(
           [&](int b, int ks) { return *reinterpret_cast<const u16x8*>(T + b * BLK + 512 * ks + 8 * lane); },
           qf, acc);
+      __builtin_amdgcn_s_setprio(0);
       TileWeights w[NB];
       bool open = true;  // every key of the tile visible to every column
 #pragma unroll
@@ -1630,6 +1635,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int nb = 0; nb < NB; ++nb)
           w[nb] = tile_softmax<D, true, WIN>(st[nb], acc[nb], j0, pos[nb], lo[nb], P.c);
       }
+      __builtin_amdgcn_s_setprio(2);
 #pragma unroll
       for (int m = 0; m < D / 16; ++m) {
         const int o = 256 * m + 4 * lane;
@@ -1640,6 +1646,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) tile_commit<D>(st[nb], w[nb]);
+      __builtin_amdgcn_s_setprio(0);
     }
     if (kt % kTilesPerSplit == kTilesPerSplit - 1 || kt == ntiles - 1) {
       // split k ends: fold it into the running merge for columns that have it

@@ -19,7 +19,7 @@
 // each wavefront a 64 x 96 part (4 x 6 MFMA blocks of 16 x 16).  K advances
 // in steps of 64 through a 2-stage LDS ring of A and B tiles (256 and 192
 // rows x 64 values; 112 KB, one workgroup and two wavefronts per SIMD on a
-// CU) filled by direct global-to-LDS copies; the 16-byte chunks of each
+// CU) filled by direct global-to-LDS copies, with one barrier per step; the 16-byte chunks of each
 // 128-byte LDS row are XOR-swizzled by the row so that the 16 rows one operand
 // read touches fall in different banks.  Tiles are taken in groups of 4 row
 // tiles sweeping the column tiles, and each XCD (workgroup id mod 8) takes a
@@ -136,16 +136,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int y = 0; y < kYB; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // One barrier per step: after it, step t's copies are visible to every
+  // wavefront and every wavefront is done with step t - 1, whose stage the
+  // copies of step t + 1 then refill while step t is computed.
   const int steps = K / kBK;
   if (steps > 0) fetch(0, 0);
   for (int t = 0; t < steps; ++t) {
-    if (t + 1 < steps) {
-      fetch(t + 1, (t + 1) & 1);
-      wait_vmcnt<kCopiesA + kCopiesB>();  // this wavefront's copies of step t have landed
-    } else {
-      wait_vmcnt<0>();
-    }
-    lds_barrier();  // every wavefront's copies of step t have landed
+    wait_vmcnt<0>();  // this wavefront's copies of step t have landed
+    lds_barrier();
+    if (t + 1 < steps) fetch(t + 1, (t + 1) & 1);
     const char* TA = reinterpret_cast<const char*>(lds) + (t & 1) * kStageBytes;
     const char* TB = TA + kTileA;
 #pragma unroll
@@ -163,7 +162,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int y = 0; y < kYB; ++y) acc[x][y] = mfma(af[x], bf[y], acc[x][y]);
     }
-    lds_barrier();  // every wavefront is done with stage t & 1 before it is refilled
   }
 
   // accumulator cell i of block (x, y) in lane (col, grp): row 16 x + 4 grp + i, column 16 y + col
