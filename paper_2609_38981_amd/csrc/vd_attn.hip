@@ -2122,10 +2122,9 @@ int run_prefix(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr) {
                         std::min(kCascMaxSplits, std::max(P.max_splits - 1, 1));
   const int64_t blocks = (std::min<int64_t>(bound, 2 * 256) + 7) / 8 * 8;
   constexpr size_t lds = prefix_lds_bytes<D>();
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&prefix_kernel<D>), hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)lds);
-  if (attr != hipSuccess) return VD_ERR_LAUNCH;
+  static std::atomic<unsigned char> lds_set[kMaxDevices];
+  if (set_lds_limit(reinterpret_cast<const void*>(&prefix_kernel<D>), (int)lds, lds_set) != hipSuccess)
+    return VD_ERR_LAUNCH;
   hipExtLaunchKernelGGL((prefix_kernel<D>), dim3((unsigned)blocks), dim3(256), (uint32_t)lds, s, e0,
                         nullptr, 0, P);
   return launched();
@@ -2175,13 +2174,9 @@ int run_chunks(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent
   constexpr size_t lds = chunk_lds_bytes<D>();
   // a handle's window is fixed at creation: one kernel per handle
   const auto kern = P.window > 0 ? &chunk_kernel<D, true> : &chunk_kernel<D, false>;
-  static const hipError_t attr0 = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&chunk_kernel<D, false>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  static const hipError_t attr1 = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&chunk_kernel<D, true>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (attr0 != hipSuccess || attr1 != hipSuccess) return VD_ERR_LAUNCH;
+  static std::atomic<unsigned char> lds_set[2][kMaxDevices];
+  if (set_lds_limit(reinterpret_cast<const void*>(kern), (int)lds, lds_set[P.window > 0]) != hipSuccess)
+    return VD_ERR_LAUNCH;
   hipExtLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), (uint32_t)lds, s, e0, e1, 0, P);
   return launched();
 }

@@ -1,10 +1,13 @@
 // vd_hw.hpp -- gfx950 helpers shared by the library's kernels: wave-uniform
-// values, vector-memory wait counts, direct global-to-LDS copies and an
-// LDS-only workgroup barrier.  No arithmetic of any result lives here.
+// values, vector-memory wait counts, direct global-to-LDS copies, unpaired
+// LDS reads, an LDS-only workgroup barrier, and the host's per-device LDS
+// limit.  No arithmetic of any result lives here.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <atomic>
 
 namespace vd {
 
@@ -51,6 +54,23 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Host: raises a kernel's dynamic LDS limit to `bytes` on the current device,
+// once per (call site, device).  The attribute belongs to the device, and a
+// process may drive several GPUs; `done` is the call site's own flag array.
+// Two threads may both set it the first time, which is harmless.
+constexpr int kMaxDevices = 64;
+inline hipError_t set_lds_limit(const void* fn, int bytes,
+                                std::atomic<unsigned char> (&done)[kMaxDevices]) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const bool tracked = dev >= 0 && dev < kMaxDevices;
+  if (tracked && done[dev].load(std::memory_order_acquire)) return hipSuccess;
+  e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && tracked) done[dev].store(1, std::memory_order_release);
+  return e;
 }
 
 }  // namespace vd

@@ -197,10 +197,9 @@ extern "C" int vd_linear(const void* a, int64_t lda, const void* b, int64_t ldb,
   const int64_t total = tiles_m * tiles_n;
   const int64_t blocks = (total + 7) / 8 * 8;
   if (tiles_m > INT32_MAX || blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&linear_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-      kLinLds);
-  if (attr != hipSuccess) return VD_ERR_LAUNCH;
+  static std::atomic<unsigned char> lds_set[kMaxDevices];
+  if (set_lds_limit(reinterpret_cast<const void*>(&linear_kernel), kLinLds, lds_set) != hipSuccess)
+    return VD_ERR_LAUNCH;
   hipLaunchKernelGGL(linear_kernel, dim3((unsigned)blocks), dim3(kThreads), kLinLds, stream,
                      static_cast<const uint16_t*>(a), lda, static_cast<const uint16_t*>(b), ldb,
                      static_cast<uint16_t*>(c), ldc, M, N, K, (int)tiles_m, (int)tiles_n);
