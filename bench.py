@@ -297,9 +297,8 @@ def main():
                          "and writes that many bytes) before timing, to calibrate HBM counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the kernel is "
-              "shown on one GPU's share; see the sharding notes). Run with --gpus 1.",
-              file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (the kernels "
+              "run on one GPU's share of the work). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
