@@ -353,14 +353,14 @@ def main():
     # each replica's call marshalled once: a phase is then a single C call
     prepared = [attn.prepare(dc.batch, out, ws, stream) for dc, ws, out in reps]
 
-    def step(i, ev=None, all_ev=None):
+    def step(i, ev=None, all_ev=None, timed=None):
         pc = prepared[i % len(prepared)]
         phases = [pc.plan, pc.splits, pc.chunks, pc.merge]
         names = ["plan_and_kv_write", "splits", "chunks", "merge"]
         for j, (name, fn) in enumerate(zip(names, phases)):
             if all_ev is not None:
                 all_ev[j].record(stream)
-            if ev is not None and name == dominant:
+            if ev is not None and name == (timed or dominant):
                 fn(events=ev)  # recorded by the kernel's own dispatch
             else:
                 fn()
@@ -404,20 +404,36 @@ def main():
         "plan+kv_write %.4f splits %.4f chunks %.4f merge %.4f"
         % (ms, enqueued * 1e3 / args.steps, dominant, dom_ms, *ph_ms))
 
+    # outside the timed region: a call with both kinds of rows also times the
+    # other phase's kernel by its own dispatches
+    other = "chunks" if dominant == "splits" else "splits"
+    other_ms = None
+    if chunk_flops > 0 and split_reqs:
+        oev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(8)]
+        for pair in oev:
+            for e in pair:
+                e.record(stream)
+        torch.cuda.synchronize()
+        for i in range(len(oev)):
+            step(i, ev=oev[i], timed=other)
+        torch.cuda.synchronize()
+        other_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in oev]))
+
     kv_bytes = call.kv_bytes()
     uniq_bytes = call.unique_kv_bytes()
     T = call.total_q_tokens
     hq, hkv, D = sh.num_q_heads, sh.num_kv_heads, sh.head_dim
     value = kv_bytes / (ms * 1e-3) / 1e9
-    if dominant == "chunks":
-        ach = chunk_flops / (dom_ms * 1e-3) / 1e12
-        roof = {"kernel": "chunk_kernel", "bound": "mfma", "achieved": round(ach, 3),
-                "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": round(ach / MFMA_BF16_PEAK_TFS, 4),
-                "traffic": measured_traffic("chunk_kernel", args.workload),
-                "avg_ms": round(dom_ms, 5), "timed_launches": len(evs),
-                "algorithmic_flop": int(chunk_flops)}
-    else:
+
+    def roofline(kind, k_ms, launches):
+        if kind == "chunks":
+            ach = chunk_flops / (k_ms * 1e-3) / 1e12
+            return {"kernel": "chunk_kernel", "bound": "mfma", "achieved": round(ach, 3),
+                    "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                    "frac": round(ach / MFMA_BF16_PEAK_TFS, 4),
+                    "traffic": measured_traffic("chunk_kernel", args.workload),
+                    "avg_ms": round(k_ms, 5), "timed_launches": launches,
+                    "algorithmic_flop": int(chunk_flops)}
         # K+V of the visible keys, Q, the page-table entries read; and when the
         # split items write the call's new tokens themselves (every row on the
         # split path, at most 16 query rows per request, at most 256 requests),
@@ -426,18 +442,20 @@ def main():
             sum(-(-r.n // P) - call.first_key(i) // P for i, r in zip(split_idx, split_reqs)) * 4
         if len(split_reqs) == call.num_seqs <= 256 and call.max_q_len <= 16:
             alg += 2 * T * hkv * D * 2 * 2
-        ach = alg / (dom_ms * 1e-3) / 1e9
+        ach = alg / (k_ms * 1e-3) / 1e9
         # with the shared_pages hint the library's shared-prefix pass runs
         # (no window, 2 .. 1024 requests, contexts past one split): the timed
         # phase is the shared-prefix kernel and the split kernel together
         casc = bool(reps[0][0].batch.shared_pages) and sh.window == 0 and \
             2 <= call.num_seqs <= 1024 and call.max_context_len > V.SPLIT_KEYS
-        roof = {"kernel": "prefix_kernel+split_kernel" if casc else "split_kernel",
+        return {"kernel": "prefix_kernel+split_kernel" if casc else "split_kernel",
                 "bound": "hbm", "achieved": round(ach, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic("split_kernel", args.workload),
-                "avg_ms": round(dom_ms, 5), "timed_launches": len(evs),
+                "avg_ms": round(k_ms, 5), "timed_launches": launches,
                 "algorithmic_bytes": int(alg)}
+
+    roof = roofline(dominant, dom_ms, len(evs))
 
     res = {
         "metric": "paged-attn KV GB/s (% HBM peak) at bitwise batch/chunk/page invariance",
@@ -465,6 +483,10 @@ def main():
                                 zip(["plan_and_kv_write", "splits", "chunks", "merge"], ph_ms)},
         "roofline": roof,
     }
+    if other_ms is not None:
+        # the other kind of rows' kernel (the dominant one is the kernel whose
+        # ideal time on its own roofline is the longer)
+        res["roofline_other_kernel"] = roofline(other, other_ms, len(oev))
     # outside the timed region: the output of the timed call, and the first and
     # last requests run alone, whose rows must be bit-identical to the batched ones
     gpu_bits = S.bits_of(reps[0][2])
