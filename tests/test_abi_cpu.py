@@ -108,3 +108,28 @@ def test_forward_rejects_before_launch(lib):
     assert lib.vd_kv_write(h, None, fake, fake, 3, fake, fake, 4, None) == -1
     assert lib.vd_kv_write(h, fake, fake, fake, 0, fake, fake, 4, None) == 0
     lib.vd_attn_destroy(h)
+
+
+def test_linear_rejects_before_launch(lib):
+    """vd_linear's host checks: every case returns before a kernel is launched."""
+    fake = 0x1000  # 16-byte aligned, never dereferenced
+    f = lib.vd_linear
+    i64, i32 = ctypes.c_int64, ctypes.c_int32
+    ok = dict(a=fake, lda=64, b=fake, ldb=64, c=fake, ldc=16, M=4, N=16, K=64)
+
+    def call(**kw):
+        d = dict(ok)
+        d.update(kw)
+        return f(ctypes.c_void_p(d["a"]), i64(d["lda"]), ctypes.c_void_p(d["b"]), i64(d["ldb"]),
+                 ctypes.c_void_p(d["c"]), i64(d["ldc"]), i64(d["M"]), i32(d["N"]), i32(d["K"]),
+                 None)
+
+    # an empty output is a no-op
+    assert call(M=0) == 0 and call(N=0) == 0
+    # negative sizes, a missing or too narrow output, misaligned rows or pointers
+    for kw in (dict(M=-1), dict(N=-1), dict(K=-1), dict(c=0), dict(ldc=8), dict(c=fake + 1),
+               dict(a=0), dict(b=0), dict(lda=32), dict(ldb=32), dict(lda=68), dict(ldb=68),
+               dict(a=fake + 8), dict(b=fake + 8)):
+        assert call(**kw) == -1, kw
+    # K must be a multiple of the 64-wide step
+    assert call(K=96, lda=96, ldb=96) == -2
