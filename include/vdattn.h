@@ -40,8 +40,14 @@
  * ------
  * Every entry point returns VD_OK (0) or a negative vd_status.  Arguments the
  * host can see are checked before anything is launched; on such an error no
- * output is touched.  Device-side data (lengths, page ids) is not read by the
- * host; the kernels never access memory outside the buffers described below:
+ * output is touched.  Among them, alignment (VD_ERR_INVALID_ARG otherwise):
+ * the bf16 buffers (q, k_pool, v_pool, k_new, v_new, the output) and the
+ * workspace start at a multiple of 16 bytes, the int32 and fp32 arrays
+ * (cu_q_lens, context_lens, page_table, lse, a validator's status) at a
+ * multiple of 4, vd_kv_write's slot_mapping at a multiple of 8; the kernels
+ * access them with aligned vector loads and stores.  Device-side data
+ * (lengths, page ids) is not read by the host; the kernels never access
+ * memory outside the buffers described below:
  * a request whose lengths violate 0 < s <= n, whose page count exceeds the
  * table stride, whose lengths exceed the hints, or whose rows fall outside
  * total_q_tokens is skipped (its output rows are left unwritten), and a page
@@ -230,11 +236,11 @@ int vd_pool_bytes(const vd_attn* h, int64_t num_pages, size_t* bytes);
 /* KV-cache write (the engine writes new tokens' K/V to private slots before
  * attention reads them, Section 4.1 "Separate cache reuse from generation").
  *
- * k_new, v_new: device [num_tokens, Hkv, D] bf16 rows.
- * slot_mapping: device [num_tokens] int64, slot = page * 16 + offset; a
+ * k_new, v_new: device [num_tokens, Hkv, D] bf16 rows (16-byte aligned).
+ * slot_mapping: device [num_tokens] int64 (8-byte aligned), slot = page * 16 + offset; a
  *               negative slot skips the token; slots outside
  *               [0, num_pages * 16) are skipped too.
- * k_pool, v_pool: device pools of vd_pool_bytes(num_pages) bytes each.
+ * k_pool, v_pool: device pools of vd_pool_bytes(num_pages) bytes each (16-byte aligned).
  *
  * Pool layout (one "page block" per (page, KV head), 16 * D bf16 elements at
  * element offset (page * Hkv + kv_head) * 16 * D):

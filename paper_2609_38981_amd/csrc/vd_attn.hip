@@ -66,6 +66,9 @@ struct Params {
   int32_t num_pages;  // page ids are int32: pages past INT32_MAX are unreachable
   int num_seqs, pt_stride, max_q, max_ctx, max_splits, split_cols;
   int hq, hkv, G;
+  // the dies workgroups are dispatched over (workgroup b on die b mod xcds,
+  // xcds = 1 << xcd_shift); item ranges are assigned per die
+  int xcds, xcd_shift;
   int window;  // sliding window in keys (Appendix A.5), 0 = the full causal prefix
   float c;  // softmax scale * log2(e), rounded once to fp32 on the host
   // optional K/V of the call's query rows ([T, Hkv, D]), written into the pool
@@ -382,7 +385,7 @@ __host__ __device__ __forceinline__ int64_t split_slots(const Params& P) {
 // its first K/V loads after a single scalar load.  r = -1 marks an unused slot.
 constexpr int kItemInts = 8;  // {r, g, k, n, q0, s, half, 0}
 // Number of counters of the planning scan: whole splits, chunk q-tiles, and
-// the last (partial) splits by their tile count, 8 down to 1.
+// the last (partial) splits by their tile count, 16 down to 1.
 constexpr int kPlanCounters = 2 + kTilesPerSplit;
 
 __device__ __forceinline__ void put_item(const Params& P, int64_t idx, int r, int g, int k,
@@ -614,7 +617,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
   // Pass 1: prefix offsets.  Split items: every whole split, then the last
   // partial splits ordered by decreasing tile count (longest first), so that
   // the items that start late in the launch are the shortest.  Counter 0:
-  // whole-split items; 1: chunk q-tiles per KV head; 2 + 8 - t: requests whose
+  // whole-split items; 1: chunk q-tiles per KV head; 2 + 16 - t: requests whose
   // last split has t tiles (Hkv items each), counted with ballots.
   for (int r0 = 0; r0 < P.num_seqs; r0 += 1024) {
     const int r = r0 + tid;
@@ -1023,10 +1026,11 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 // requests): every workgroup reads all requests' lengths in one round trip
 // (lane l holds requests l, 64 + l, ...) and derives its own item.  Items are
 // listed per KV head -- every whole 1024-key split (requests ascending, splits
-// ascending), then every last partial split, longest first (tile count 8 down
-// to 1, requests ascending) -- and each XCD (workgroup id mod 8) takes a
-// contiguous range of the list: with 8 KV heads XCD x runs head x, so a page
-// read by several requests stays in one L2, and within an XCD the shortest
+// ascending), then every last partial split, longest first (tile count 16 down
+// to 1, requests ascending) -- and each die (XCD: workgroup id mod the
+// die count, 8 on a whole MI355X) takes a contiguous range of the list: with
+// 8 KV heads and 8 dies XCD x runs head x, so a page read by several requests
+// stays in one L2, and within an XCD the shortest
 // items start last.
 constexpr int kInWaveChunks = 4;
 constexpr int kInWaveMaxSeqs = 64 * kInWaveChunks;
@@ -1034,7 +1038,7 @@ constexpr int kInWaveMaxSeqs = 64 * kInWaveChunks;
 struct SplitRef {
   int r, g, k, half;
   Req R;
-  int per_xcd;  // items each XCD takes (slots b with b / 8 < per_xcd hold one)
+  int per_xcd;  // items each XCD takes (slots b with b / xcds < per_xcd hold one)
 };
 
 // Inclusive prefix sum over the 64 lanes with DPP moves: shifts by 1, 2, 4
@@ -1099,11 +1103,11 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
     partial += __popcll(__ballot(cls[c] > 0)) + __popcll(__ballot(cls[c] > 0 && hv[c] == 2));
   const int per_head = whole + partial;
   const int total = per_head * P.hkv;
-  const int per_xcd = (total + 7) / 8;
+  const int per_xcd = (total + P.xcds - 1) >> P.xcd_shift;
   out.per_xcd = per_xcd;
-  const int jx = vb / 8;
+  const int jx = vb >> P.xcd_shift;
   if (jx >= per_xcd) return false;
-  const int i = (vb % 8) * per_xcd + jx;
+  const int i = (vb & (P.xcds - 1)) * per_xcd + jx;
   if (i >= total) return false;
   out.g = uni(i / per_head);
   int idx = i - out.g * per_head;
@@ -1203,10 +1207,10 @@ __device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& 
     per_head += __builtin_amdgcn_readlane(incl[c], 63);
   }
   const int total = per_head * P.hkv;
-  const int per_xcd = (total + 7) / 8;
-  const int jx = (int)(blockIdx.x / 8);
+  const int per_xcd = (total + P.xcds - 1) >> P.xcd_shift;
+  const int jx = (int)(blockIdx.x >> P.xcd_shift);
   if (jx >= per_xcd) return false;
-  const int i = (int)(blockIdx.x % 8) * per_xcd + jx;
+  const int i = (int)(blockIdx.x & (P.xcds - 1)) * per_xcd + jx;
   if (i >= total) return false;
   g = uni(i / per_head);
   const int rem = i - g * per_head;
@@ -1243,7 +1247,7 @@ __device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& 
 // end of the launch short when item durations vary.  The grid is capped at
 // about twice the wavefronts the chip holds at once; workgroup b
 // takes the slots b, b + grid, b + 2 grid, ... (the grid is a multiple of the
-// 8 XCDs, so its slots stay on its XCD) until one is past the items.  NT:
+// dies, so its slots stay on its XCD) until one is past the items.  NT:
 // K/V are streamed with non-temporal loads.
 template <int D, bool WIN, bool NT>
 __global__ __launch_bounds__(64) void split_kernel(Params P) {
@@ -1283,7 +1287,7 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
       R.valid = true;
     }
     split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds, half);
-    if (P.inwave && (vb + (int)gridDim.x) / 8 >= per_xcd) return;  // no further slot holds an item
+    if (P.inwave && ((vb + (int)gridDim.x) >> P.xcd_shift) >= per_xcd) return;  // no further slot holds an item
   }
 }
 
@@ -1474,9 +1478,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int col = lane & 15;
   const int window = WIN ? P.window : 0;
   // Items are ordered (KV head, request, q-tile) and blocks of one XCD (block
-  // id mod 8) take a contiguous range of them: the q-tiles of one (request,
-  // KV head) share that XCD's L2, and with 8 KV heads each XCD takes one head
-  // of every request, so long and short requests spread over all XCDs.
+  // id mod the die count) take a contiguous range of them: the q-tiles of one
+  // (request, KV head) share that XCD's L2, and with 8 KV heads on 8 dies each
+  // XCD takes one head of every request, so long and short requests spread
+  // over all XCDs.
   int g, r, qt;
   Req R;
   if (P.inwave) {
@@ -1484,10 +1489,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   } else {
     const int per_head = P.off_chunk[P.num_seqs];
     const int total = per_head * P.hkv;
-    const int per_xcd = (total + 7) / 8;
-    const int jx = (int)(blockIdx.x / 8);
+    const int per_xcd = (total + P.xcds - 1) >> P.xcd_shift;
+    const int jx = (int)(blockIdx.x >> P.xcd_shift);
     if (jx >= per_xcd) return;
-    const int i = uni((int)(blockIdx.x % 8) * per_xcd + jx);
+    const int i = uni((int)(blockIdx.x & (P.xcds - 1)) * per_xcd + jx);
     if (i >= total) return;
     g = uni(i / per_head);
     const int rem = i - g * per_head;
@@ -1870,7 +1875,7 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
 }
 
 // Items: KV head major, then listed group, then (tile, split).  Each XCD
-// (workgroup id mod 8) takes a contiguous eighth of the list, which its
+// (workgroup id mod the die count) takes a contiguous share of the list, which its
 // workgroups run in turn: the grid is sized to the chip, not to the list.
 template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefix_kernel(Params P) {
@@ -1880,9 +1885,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int ngroups = P.casc_hdr[0], per_head = P.casc_hdr[1];
   if (ngroups < 1 || ngroups > P.num_seqs / 2 || per_head < 1 || per_head > (1 << 24)) return;
   const int total = per_head * P.hkv;
-  const int per_xcd = (total + 7) / 8;
-  for (int j = (int)(blockIdx.x / 8); j < per_xcd; j += (int)(gridDim.x / 8)) {
-    const int i = uni((int)(blockIdx.x % 8) * per_xcd + j);
+  const int per_xcd = (total + P.xcds - 1) >> P.xcd_shift;
+  for (int j = (int)(blockIdx.x >> P.xcd_shift); j < per_xcd; j += (int)(gridDim.x >> P.xcd_shift)) {
+    const int i = uni((int)(blockIdx.x & (P.xcds - 1)) * per_xcd + j);
     if (i >= total) break;
     prefix_item<D>(P, i, ngroups, per_head, lds, scu);
     __syncthreads();  // LDS (ring, scu) is free for the next item
@@ -1980,6 +1985,9 @@ WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_context_len) 
   return L;
 }
 
+// p is a multiple of a bytes (a null pointer is).
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
 int check_batch(const vd_attn* h, const vd_attn_batch* b) {
   if (!h || !b) return VD_ERR_INVALID_ARG;
   if (b->num_seqs < 0 || b->total_q_tokens < 0) return VD_ERR_INVALID_ARG;
@@ -1991,6 +1999,21 @@ int check_batch(const vd_attn* h, const vd_attn_batch* b) {
   if (b->max_q_len > b->max_context_len) return VD_ERR_INVALID_ARG;
   if (b->total_q_tokens > INT32_MAX) return VD_ERR_INVALID_ARG;
   if ((b->k_new == nullptr) != (b->v_new == nullptr)) return VD_ERR_INVALID_ARG;
+  // the kernels read and write these buffers with aligned vector accesses
+  // (16 bytes for bf16 data, 4 for int32 and fp32 entries)
+  if (!aligned(b->q, 16) || !aligned(b->k_pool, 16) || !aligned(b->v_pool, 16) ||
+      !aligned(b->k_new, 16) || !aligned(b->v_new, 16) || !aligned(b->cu_q_lens, 4) ||
+      !aligned(b->context_lens, 4) || !aligned(b->page_table, 4) || !aligned(b->lse, 4))
+    return VD_ERR_INVALID_ARG;
+  return VD_OK;
+}
+
+// The output (16-byte aligned, like the other bf16 buffers) and the workspace
+// (16-byte aligned: its fields are read and written as 16-byte vectors, and
+// its offsets are multiples of 256 bytes from its start).
+int check_out_ws(const void* out, bool need_out, const void* ws) {
+  if (need_out && !out) return VD_ERR_INVALID_ARG;
+  if (!aligned(out, 16) || !aligned(ws, 16)) return VD_ERR_INVALID_ARG;
   return VD_OK;
 }
 
@@ -2056,6 +2079,9 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.hq = h->hq;
   P.hkv = h->hkv;
   P.G = h->group;
+  const Geometry geo = device_geometry();
+  P.xcds = geo.xcds;
+  P.xcd_shift = geo.xcd_shift;
   P.window = h->window;
   P.c = h->c;
   P.knew = static_cast<const uint16_t*>(b->k_new);
@@ -2101,10 +2127,11 @@ int run_splits(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e0 = n
   // themselves take XCD-contiguous ranges of the items.
   const int64_t items = split_slots(P);
   if (items > INT32_MAX - 8) return VD_ERR_INVALID_ARG;
-  // at most about twice the wavefronts the chip holds at once (1024 SIMDs,
-  // two wavefronts each); a multiple of 8
-  const int64_t cap = 4096;
-  const dim3 grid((unsigned)((std::min(items, cap) + 7) / 8 * 8)), block(64);
+  // at most about twice the wavefronts the chip holds at once (4 SIMDs per
+  // compute unit, two wavefronts each); a multiple of the dies
+  const Geometry geo = device_geometry();
+  const int64_t cap = 16 * (int64_t)geo.cus;
+  const dim3 grid((unsigned)((std::min(items, cap) + geo.xcds - 1) / geo.xcds * geo.xcds)), block(64);
   const auto kern = stream_kv ? split_kernel_for<D, true>(P) : split_kernel_for<D, false>(P);
   hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, P);
   return launched();
@@ -2112,15 +2139,17 @@ int run_splits(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e0 = n
 
 template <int D>
 int run_prefix(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr) {
-  // Two workgroups per CU (256 CUs), or fewer for fewer items: an upper
-  // bound of the items is Hkv (ceil(T G / 128) + B / 2) tiles (the members'
-  // query rows of different groups are disjoint, and a listed group has at
-  // least two requests) times the shared splits, at most max_splits - 1.
-  // A multiple of the 8 XCDs.
+  // Two workgroups per CU, or fewer for fewer items: an upper bound of the
+  // items is Hkv (ceil(T G / 128) + B / 2) tiles (the members' query rows of
+  // different groups are disjoint, and a listed group has at least two
+  // requests) times the shared splits, at most max_splits - 1.  A multiple
+  // of the dies.
   const int64_t bound = (int64_t)P.hkv *
                         ((P.T * P.G + kChunkCols - 1) / kChunkCols + P.num_seqs / 2) *
                         std::min(kCascMaxSplits, std::max(P.max_splits - 1, 1));
-  const int64_t blocks = (std::min<int64_t>(bound, 2 * 256) + 7) / 8 * 8;
+  const Geometry geo = device_geometry();
+  const int64_t blocks =
+      (std::min<int64_t>(bound, 2 * (int64_t)geo.cus) + geo.xcds - 1) / geo.xcds * geo.xcds;
   constexpr size_t lds = prefix_lds_bytes<D>();
   static std::atomic<unsigned char> lds_set[kMaxDevices];
   if (set_lds_limit(reinterpret_cast<const void*>(&prefix_kernel<D>), (int)lds, lds_set) != hipSuccess)
@@ -2167,9 +2196,9 @@ int run_merge(const Params& P, hipStream_t s) {
 template <int D>
 int run_chunks(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
   // upper bound of sum_r Hkv * ceil(s_r G / 128) <= Hkv (ceil(T G / 128) + B),
-  // rounded up to a multiple of the 8 XCDs
+  // rounded up to a multiple of the dies
   int64_t blocks = (int64_t)P.hkv * ((P.T * P.G + kChunkCols - 1) / kChunkCols + P.num_seqs);
-  blocks = (blocks + 7) / 8 * 8;
+  blocks = (blocks + P.xcds - 1) / P.xcds * P.xcds;
   if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
   constexpr size_t lds = chunk_lds_bytes<D>();
   // a handle's window is fixed at creation: one kernel per handle
@@ -2233,6 +2262,7 @@ int vd_attn_forward_plan(const vd_attn* h, const vd_attn_batch* b, void* workspa
                          size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
+  if ((rc = check_out_ws(nullptr, false, workspace)) != VD_OK) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   if (!needs_plan(h, b)) return VD_OK;  // the split workgroups plan for themselves
   const Params P = make_params(h, b, nullptr, workspace);
@@ -2243,7 +2273,7 @@ int vd_attn_forward_splits(const vd_attn* h, const vd_attn_batch* b, void* out, 
                            size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
-  if (!out) return VD_ERR_INVALID_ARG;
+  if ((rc = check_out_ws(out, true, workspace)) != VD_OK) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
   // with the shared-prefix pass, the shared splits are read (cached) by the
@@ -2256,7 +2286,7 @@ int vd_attn_forward_chunks(const vd_attn* h, const vd_attn_batch* b, void* out,
                            const void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
-  if (!out) return VD_ERR_INVALID_ARG;
+  if ((rc = check_out_ws(out, true, workspace)) != VD_OK) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   if (!needs_chunks(h, b)) return VD_OK;
   const Params P = make_params(h, b, out, workspace);
@@ -2276,7 +2306,7 @@ int vd_attn_forward_splits_timed(const vd_attn* h, const vd_attn_batch* b, void*
   int rc = check_batch(h, b);
   if (rc != VD_OK) return rc;
   if (b->num_seqs == 0 || b->total_q_tokens == 0) return record_pair(stream, start, stop);
-  if (!out) return VD_ERR_INVALID_ARG;
+  if ((rc = check_out_ws(out, true, workspace)) != VD_OK) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
   // with the shared-prefix pass, the shared splits are read (cached) by the
@@ -2292,7 +2322,7 @@ int vd_attn_forward_chunks_timed(const vd_attn* h, const vd_attn_batch* b, void*
   int rc = check_batch(h, b);
   if (rc != VD_OK) return rc;
   if (b->num_seqs == 0 || b->total_q_tokens == 0) return record_pair(stream, start, stop);
-  if (!out) return VD_ERR_INVALID_ARG;
+  if ((rc = check_out_ws(out, true, workspace)) != VD_OK) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   if (!needs_chunks(h, b)) return record_pair(stream, start, stop);
   const Params P = make_params(h, b, out, workspace);
@@ -2304,7 +2334,7 @@ int vd_attn_forward_merge(const vd_attn* h, const vd_attn_batch* b, void* out,
                           const void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
-  if (!out) return VD_ERR_INVALID_ARG;
+  if ((rc = check_out_ws(out, true, workspace)) != VD_OK) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   const Params P = make_params(h, b, out, workspace);
   return h->d == 64 ? run_merge<64>(P, stream) : run_merge<128>(P, stream);
@@ -2314,7 +2344,7 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* b, void* out, void* w
                     size_t workspace_bytes, hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
-  if (!out) return VD_ERR_INVALID_ARG;
+  if ((rc = check_out_ws(out, true, workspace)) != VD_OK) return rc;
   if (!ws_ok(h, b, workspace, workspace_bytes)) return VD_ERR_WORKSPACE;
   rc = vd_attn_forward_plan(h, b, workspace, workspace_bytes, stream);
   if (rc != VD_OK) return rc;
@@ -2329,7 +2359,8 @@ int vd_attn_validate(const vd_attn* h, const vd_attn_batch* b, int32_t* status,
                      hipStream_t stream) {
   int rc = check_batch(h, b);
   if (rc != VD_OK || b->num_seqs == 0) return rc;
-  if (!status || !b->cu_q_lens || !b->context_lens || !b->page_table || b->pt_stride < 1)
+  if (!status || !b->cu_q_lens || !b->context_lens || !b->page_table || b->pt_stride < 1 ||
+      !aligned(status, 4))
     return VD_ERR_INVALID_ARG;
   hipLaunchKernelGGL(validate_kernel, dim3((unsigned)b->num_seqs), dim3(64), 0, stream,
                      b->cu_q_lens, b->context_lens, b->page_table, b->pt_stride, b->num_pages,
@@ -2349,6 +2380,9 @@ int vd_kv_write(const vd_attn* h, const void* k_new, const void* v_new,
   if (!h || num_tokens < 0 || num_pages < 0) return VD_ERR_INVALID_ARG;
   if (num_tokens == 0) return VD_OK;
   if (!k_new || !v_new || !slot_mapping || !k_pool || !v_pool) return VD_ERR_INVALID_ARG;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(slot_mapping, 8) ||
+      !aligned(k_pool, 16) || !aligned(v_pool, 16))
+    return VD_ERR_INVALID_ARG;
   const int64_t threads = num_tokens * h->hkv * (h->d / 8);
   const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
   const uint16_t* kn = static_cast<const uint16_t*>(k_new);

@@ -1,7 +1,7 @@
 // vd_hw.hpp -- gfx950 helpers shared by the library's kernels: wave-uniform
 // values, vector-memory wait counts, direct global-to-LDS copies, unpaired
 // LDS reads, an LDS-only workgroup barrier, and the host's per-device LDS
-// limit.  No arithmetic of any result lives here.
+// limit and chip geometry.  No arithmetic of any result lives here.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -71,6 +71,37 @@ inline hipError_t set_lds_limit(const void* fn, int bytes,
   e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e == hipSuccess && tracked) done[dev].store(1, std::memory_order_release);
   return e;
+}
+
+// Host: the current device's geometry, read once per device.  cus: compute
+// units; xcds: the accelerator dies the dispatcher spreads workgroups over,
+// workgroup b landing on die b mod xcds (a power of two: the 32-CU dies of
+// gfx950, 8 on a whole MI355X, fewer when the GPU is partitioned).  Only
+// launch shapes and the order in which workgroups take work items depend on
+// it, never a value.
+struct Geometry {
+  int cus, xcds, xcd_shift;
+};
+
+inline Geometry device_geometry() {
+  static std::atomic<int> cache[kMaxDevices];  // cus + 1, 0: not read yet
+  constexpr int kCusPerXcd = 32;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = -1;
+  const bool tracked = dev >= 0 && dev < kMaxDevices;
+  if (tracked) cus = cache[dev].load(std::memory_order_acquire) - 1;
+  if (cus <= 0) {
+    if (dev < 0 || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                       hipSuccess || cus <= 0)
+      cus = 256;
+    if (tracked) cache[dev].store(cus + 1, std::memory_order_release);
+  }
+  Geometry g;
+  g.cus = cus;
+  g.xcd_shift = 0;
+  while (g.xcd_shift < 3 && (kCusPerXcd << (g.xcd_shift + 1)) <= cus) ++g.xcd_shift;
+  g.xcds = 1 << g.xcd_shift;
+  return g;
 }
 
 }  // namespace vd

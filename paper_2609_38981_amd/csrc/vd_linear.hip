@@ -22,9 +22,9 @@
 // CU) filled by direct global-to-LDS copies, with one barrier per step; the 16-byte chunks of each
 // 128-byte LDS row are XOR-swizzled by the row so that the 16 rows one operand
 // read touches fall in different banks.  Tiles are taken in groups of 4 row
-// tiles sweeping the column tiles, and each XCD (workgroup id mod 8) takes a
-// contiguous range of that order, so the A and B panels of its workgroups are
-// shared in its L2.
+// tiles sweeping the column tiles, and each XCD (workgroup id mod the die
+// count, 8 on a whole MI355X) takes a contiguous range of that order, so the A
+// and B panels of its workgroups are shared in its L2.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -74,17 +74,18 @@ __device__ __forceinline__ int swz(int r, int ch) {
 
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void linear_kernel(
     const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, uint16_t* c, int64_t ldc,
-    int64_t M, int N, int K, int tiles_m, int tiles_n) {
+    int64_t M, int N, int K, int tiles_m, int tiles_n, int xcd_shift) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   const int wave = uni(threadIdx.x >> 6);
   const int lane = __lane_id();
   // tile order: groups of kGroupM row tiles, each sweeping the column tiles
-  // (row tile fastest); XCD x takes the x-th contiguous eighth of the order
+  // (row tile fastest); XCD x takes the x-th contiguous share of the order
   const int64_t total = (int64_t)tiles_m * tiles_n;
-  const int64_t per_xcd = (total + 7) / 8;
-  const int64_t jx = blockIdx.x / 8;
+  const int xcds = 1 << xcd_shift;
+  const int64_t per_xcd = (total + xcds - 1) >> xcd_shift;
+  const int64_t jx = blockIdx.x >> xcd_shift;
   if (jx >= per_xcd) return;
-  const int64_t i = (int64_t)(blockIdx.x % 8) * per_xcd + jx;
+  const int64_t i = (int64_t)(blockIdx.x & (xcds - 1)) * per_xcd + jx;
   if (i >= total) return;
   const int64_t group = i / ((int64_t)kGroupM * tiles_n);
   const int64_t first_m = group * kGroupM;
@@ -195,13 +196,15 @@ extern "C" int vd_linear(const void* a, int64_t lda, const void* b, int64_t ldb,
   }
   const int64_t tiles_m = (M + kBM - 1) / kBM, tiles_n = ((int64_t)N + kBN - 1) / kBN;
   const int64_t total = tiles_m * tiles_n;
-  const int64_t blocks = (total + 7) / 8 * 8;
+  const Geometry geo = device_geometry();
+  const int64_t blocks = (total + geo.xcds - 1) / geo.xcds * geo.xcds;
   if (tiles_m > INT32_MAX || blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
   static std::atomic<unsigned char> lds_set[kMaxDevices];
   if (set_lds_limit(reinterpret_cast<const void*>(&linear_kernel), kLinLds, lds_set) != hipSuccess)
     return VD_ERR_LAUNCH;
   hipLaunchKernelGGL(linear_kernel, dim3((unsigned)blocks), dim3(kThreads), kLinLds, stream,
                      static_cast<const uint16_t*>(a), lda, static_cast<const uint16_t*>(b), ldb,
-                     static_cast<uint16_t*>(c), ldc, M, N, K, (int)tiles_m, (int)tiles_n);
+                     static_cast<uint16_t*>(c), ldc, M, N, K, (int)tiles_m, (int)tiles_n,
+                     geo.xcd_shift);
   return hipGetLastError() == hipSuccess ? VD_OK : VD_ERR_LAUNCH;
 }

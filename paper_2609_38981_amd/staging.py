@@ -34,6 +34,17 @@ class DeviceCall:
         return self.call.kv_bytes()
 
 
+def clone_device_call(dc: DeviceCall) -> DeviceCall:
+    """A device copy of a staged call: every tensor of its batch cloned on the
+    device (pools, page table, queries, lengths, optional outputs)."""
+    from dataclasses import fields, replace
+
+    b = dc.batch
+    kw = {f.name: getattr(b, f.name).clone() for f in fields(b)
+          if isinstance(getattr(b, f.name), torch.Tensor)}
+    return DeviceCall(dc.call, replace(b, **kw))
+
+
 def handle_for(shape: W.Shape) -> VdAttn:
     return VdAttn(shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.page_size,
                   window=shape.window)

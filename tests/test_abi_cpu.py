@@ -133,3 +133,51 @@ def test_linear_rejects_before_launch(lib):
         assert call(**kw) == -1, kw
     # K must be a multiple of the 64-wide step
     assert call(K=96, lda=96, ldb=96) == -2
+
+
+def test_forward_rejects_misaligned_pointers(lib):
+    """Every buffer the kernels access with vector loads must be aligned: a
+    misaligned one is rejected before any launch (VD_ERR_INVALID_ARG), on every
+    entry point that takes the batch."""
+    rc, h = _create(lib)
+    fake = 0x10000  # 16-byte aligned, never dereferenced
+    ws = ctypes.c_size_t()
+    lib.vd_attn_workspace_size(h, 1, 1, 16, ctypes.byref(ws))
+
+    def batch(**kw):
+        b = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, None, None, 0, None)
+        for k, v in kw.items():
+            setattr(b, k, v)
+        return b
+
+    # bf16 buffers at 16 bytes, int32 / fp32 arrays at 4
+    cases = [dict(q=fake + 8), dict(k_pool=fake + 2), dict(v_pool=fake + 4),
+             dict(k_new=fake + 8, v_new=fake), dict(k_new=fake, v_new=fake + 2),
+             dict(cu_q_lens=fake + 2), dict(context_lens=fake + 1), dict(page_table=fake + 2),
+             dict(lse=fake + 2)]
+    for kw in cases:
+        b = batch(**kw)
+        assert lib.vd_attn_forward(h, ctypes.byref(b), fake, fake, ws.value, None) == -1, kw
+        assert lib.vd_attn_forward_plan(h, ctypes.byref(b), fake, ws.value, None) == -1, kw
+        assert lib.vd_attn_forward_splits(h, ctypes.byref(b), fake, fake, ws.value, None) == -1, kw
+        assert lib.vd_attn_forward_chunks(h, ctypes.byref(b), fake, fake, ws.value, None) == -1, kw
+        assert lib.vd_attn_forward_merge(h, ctypes.byref(b), fake, fake, ws.value, None) == -1, kw
+        st = ctypes.c_void_p(fake)
+        assert lib.vd_attn_validate(h, ctypes.byref(b), st, None) == -1, kw
+    # the output and the workspace at 16
+    b = batch()
+    for out, w in [(fake + 8, fake), (fake, fake + 8), (fake + 2, fake + 4)]:
+        assert lib.vd_attn_forward(h, ctypes.byref(b), out, w, ws.value, None) == -1, (out, w)
+        assert lib.vd_attn_forward_splits(h, ctypes.byref(b), out, w, ws.value, None) == -1
+        assert lib.vd_attn_forward_chunks(h, ctypes.byref(b), out, w, ws.value, None) == -1
+        assert lib.vd_attn_forward_merge(h, ctypes.byref(b), out, w, ws.value, None) == -1
+    assert lib.vd_attn_forward_plan(h, ctypes.byref(b), fake + 8, ws.value, None) == -1
+    # the validator's status array at 4
+    assert lib.vd_attn_validate(h, ctypes.byref(b), ctypes.c_void_p(fake + 2), None) == -1
+    # the KV write: bf16 rows and pools at 16, slot ids at 8
+    for args in [(fake + 8, fake, fake, fake, fake), (fake, fake + 2, fake, fake, fake),
+                 (fake, fake, fake + 4, fake, fake), (fake, fake, fake, fake + 8, fake),
+                 (fake, fake, fake, fake, fake + 2)]:
+        kn, vn, sm, kp, vp = args
+        assert lib.vd_kv_write(h, kn, vn, sm, 3, kp, vp, 4, None) == -1, args
+    lib.vd_attn_destroy(h)

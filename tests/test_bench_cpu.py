@@ -59,14 +59,24 @@ def test_measured_traffic_needs_the_same_code(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     digest = bench.kernel_code_digest()
     import json
-    with open(os.path.join(prof, "hbm_traffic.json"), "w") as f:
-        json.dump({"kernel": "split_kernel", "workload": "decode8b", "bytes_per_launch": 123,
-                   "code_sha256": digest}, f)
+
+    def write(entries):
+        with open(os.path.join(prof, "hbm_traffic.json"), "w") as f:
+            json.dump({"entries": entries}, f)
+
+    e = lambda k, w, b, d=digest: dict(kernel=k, workload=w, bytes_per_launch=b, code_sha256=d)
+    write([e("split_kernel", "decode8b", 123), e("split_kernel", "longdecode8b", 456),
+           e("prefix_kernel", "verify70b", 10), e("split_kernel", "verify70b", 20),
+           e("chunk_kernel", "mixed8b", 7, "0" * 64)])
     assert bench.measured_traffic("split_kernel", "decode8b") == 123
+    assert bench.measured_traffic("split_kernel", "longdecode8b") == 456
     assert bench.measured_traffic("split_kernel", "mixed8b") is None
-    with open(os.path.join(prof, "hbm_traffic.json"), "w") as f:
-        json.dump({"kernel": "split_kernel", "workload": "decode8b", "bytes_per_launch": 123,
-                   "code_sha256": "0" * 64}, f)
+    # two kernels of one phase: the sum, only when both are covered
+    assert bench.measured_traffic("prefix_kernel+split_kernel", "verify70b") == 30
+    assert bench.measured_traffic("prefix_kernel+split_kernel", "decode8b") is None
+    # counters taken on other code
+    assert bench.measured_traffic("chunk_kernel", "mixed8b") is None
+    write([e("split_kernel", "decode8b", 123, "0" * 64)])
     assert bench.measured_traffic("split_kernel", "decode8b") is None
 
 
