@@ -151,9 +151,9 @@ typedef struct {
 
 /* Bytes of workspace one call needs for the given host-side sizes: the plan
  * (int32 arrays of about 3 num_seqs, the shared-prefix list and the split work
- * list) and, for every
- * (request, KV head, query-head row < 32, 1024-key split < ceil(max_context_len /
- * 1024)), a partial state of head_dim + 2 floats. */
+ * list) and, for every (request, KV head, query-head row < min(max_q_len *
+ * Hq / Hkv, 32), 1024-key split < ceil(max_context_len / 1024)), a partial
+ * state of head_dim + 2 floats. */
 int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
                            int32_t max_context_len, size_t* bytes);
 

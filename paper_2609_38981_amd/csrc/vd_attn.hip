@@ -65,6 +65,9 @@ struct Params {
   int64_t T;
   int32_t num_pages;  // page ids are int32: pages past INT32_MAX are unreachable
   int num_seqs, pt_stride, max_q, max_ctx, max_splits, split_cols;
+  // partial states per (request, KV head, split): one per query-head row of
+  // the split path, min(max_q * G, 32) of them (the layout's column stride)
+  int ws_cols;
   int hq, hkv, G;
   // the dies workgroups are dispatched over (workgroup b on die b mod xcds,
   // xcds = 1 << xcd_shift); item ranges are assigned per die
@@ -1011,7 +1014,7 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
   for (int nb = 0; nb < NA; ++nb) {
     const int c = cbase + nb * 16 + col;
     if (pos[nb] < 0 || k > pos[nb] / kSplitKeys || k < lo[nb] / kSplitKeys) continue;
-    const int64_t pidx = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * MS + k;
+    const int64_t pidx = ((int64_t)(r * P.hkv + g) * P.ws_cols + c) * MS + k;
     if (grp == 0) {
       P.ws_m[pidx] = st[nb].m;
       P.ws_z[pidx] = st[nb].z;
@@ -1318,7 +1321,7 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   const int pr = R.n - R.s + c / P.G;
   const int klo = window_lo(pr, P.window) / kSplitKeys;
   const int kp = pr / kSplitKeys + 1 - klo;
-  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * P.max_splits + klo;
+  const int64_t p0 = ((int64_t)(r * P.hkv + g) * P.ws_cols + c) * P.max_splits + klo;
   // every partial state is loaded first, then folded in ascending split order
   float mk[KS], zk[KS];
   f32x4 uk[KS];
@@ -1384,7 +1387,7 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
   const int pr = R.n - R.s + c / P.G;
   const int klo = window_lo(pr, P.window) / kSplitKeys;
   const int kp = pr / kSplitKeys + 1 - klo;
-  const int64_t p0 = ((int64_t)(r * P.hkv + g) * kSplitCols + c) * P.max_splits + klo;
+  const int64_t p0 = ((int64_t)(r * P.hkv + g) * P.ws_cols + c) * P.max_splits + klo;
   float carry = -__builtin_inff();  // running maximum before the chunk
   float Z = 0.f, W = 0.f;
   for (int k0 = 0; k0 < kp; k0 += CH) {
@@ -1773,8 +1776,8 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
       const int r = r0 + lo;
       const int cl = (t - scu[lo]) * P.G + hh;  // the column's index among its request's
       // a member (its rows are on the split path), and the row is its own
-      v = P.casc_seq[r] == cg && t >= scu[lo] && t < scu[lo + 1] && cl < kSplitCols;
-      pidx[nb] = ((int64_t)(r * P.hkv + g) * kSplitCols + cl) * P.max_splits + k;
+      v = P.casc_seq[r] == cg && t >= scu[lo] && t < scu[lo + 1] && cl < P.ws_cols;
+      pidx[nb] = ((int64_t)(r * P.hkv + g) * P.ws_cols + cl) * P.max_splits + k;
     }
     live[nb] = v;
     load_q<D>(P, qf[nb], v ? t : 0, g * P.G + (v ? hh : 0), v);
@@ -1959,14 +1962,21 @@ struct WsLayout {
       z_off, u_off, total;
 };
 
+// Query-head rows per (request, KV head) that can hold split partial states:
+// those of a request on the split path, at most min(max_q_len * G, 32).
+int ws_cols(const vd_attn* h, int32_t max_q_len) {
+  return (int)std::min<int64_t>((int64_t)std::max(max_q_len, 1) * h->group, kSplitCols);
+}
+
 // Workspace: three offset arrays of num_seqs + 1 int32, the shared-prefix
 // plan (a header, one int32 per request, and per listed group -- at most
 // num_seqs / 2 -- an item offset and 4 int32), the split work list (8 int32
 // per (request, KV head, split, column half)), then the split partial states
-// (m, z, U) for every (request, KV head, column < 32, split).
-WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_context_len) {
+// (m, z, U) for every (request, KV head, column < ws_cols, split).
+WsLayout ws_layout(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
+                   int32_t max_context_len) {
   const int64_t ms = ((int64_t)max_context_len + kSplitKeys - 1) / kSplitKeys;
-  const int64_t n = (int64_t)num_seqs * h->hkv * kSplitCols * (ms < 1 ? 1 : ms);
+  const int64_t n = (int64_t)num_seqs * h->hkv * ws_cols(h, max_q_len) * (ms < 1 ? 1 : ms);
   const size_t offs = round_up((size_t)(num_seqs + 1) * sizeof(int32_t));
   const size_t groups = (size_t)num_seqs / 2 + 1;
   WsLayout L;
@@ -2059,7 +2069,7 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.kpool = static_cast<const uint16_t*>(b->k_pool);
   P.vpool = static_cast<const uint16_t*>(b->v_pool);
   P.out = static_cast<uint16_t*>(out);
-  const WsLayout L = ws_layout(h, b->num_seqs, b->max_context_len);
+  const WsLayout L = ws_layout(h, b->num_seqs, b->max_q_len, b->max_context_len);
   char* w = static_cast<char*>(const_cast<void*>(ws));
   P.off_full = reinterpret_cast<int32_t*>(w + L.off_full);
   P.off_part = reinterpret_cast<int32_t*>(w + L.off_part);
@@ -2076,6 +2086,7 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.max_ctx = b->max_context_len;
   P.max_splits = (b->max_context_len + kSplitKeys - 1) / kSplitKeys;
   P.split_cols = 16 * split_nb(h, b->max_q_len);
+  P.ws_cols = ws_cols(h, b->max_q_len);
   P.hq = h->hq;
   P.hkv = h->hkv;
   P.G = h->group;
@@ -2175,7 +2186,7 @@ int run_split_phase(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e
 
 template <int D>
 int run_merge(const Params& P, hipStream_t s) {
-  const int64_t cols = std::min<int64_t>((int64_t)P.max_q * P.G, P.split_cols);
+  const int64_t cols = P.ws_cols;  // = min(max_q * G, split_cols)
   if (P.max_splits <= kShortMerge) {
     const int64_t threads = (int64_t)P.num_seqs * P.hkv * cols * (D / 4);
     const int64_t blocks = (threads + 255) / 256;
@@ -2211,7 +2222,7 @@ int run_chunks(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent
 }
 
 bool ws_ok(const vd_attn* h, const vd_attn_batch* b, const void* ws, size_t bytes) {
-  return ws && bytes >= ws_layout(h, b->num_seqs, b->max_context_len).total;
+  return ws && bytes >= ws_layout(h, b->num_seqs, b->max_q_len, b->max_context_len).total;
 }
 
 }  // namespace
@@ -2254,7 +2265,7 @@ int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len
                            int32_t max_context_len, size_t* bytes) {
   if (!h || !bytes || num_seqs < 0 || max_q_len < 0 || max_context_len < 0)
     return VD_ERR_INVALID_ARG;
-  *bytes = ws_layout(h, num_seqs, max_context_len).total;
+  *bytes = ws_layout(h, num_seqs, max_q_len, max_context_len).total;
   return VD_OK;
 }
 

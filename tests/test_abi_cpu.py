@@ -64,10 +64,13 @@ def test_status_strings(lib):
 def test_workspace_and_pool_sizes(lib):
     rc, h = _create(lib)
     n = ctypes.c_size_t()
-    assert lib.vd_attn_workspace_size(h, 64, 1, 4096, ctypes.byref(n)) == 0
+    assert lib.vd_attn_workspace_size(h, 64, 8, 4096, ctypes.byref(n)) == 0
     # m, z and U (D floats) per (request, KV head, 32 columns, 4 splits of 1024 keys)
     entries = 64 * 8 * 32 * 4
     assert n.value >= entries * (2 + 128) * 4
+    # single-token rows of 4 query heads per KV head: 4 columns
+    assert lib.vd_attn_workspace_size(h, 64, 1, 4096, ctypes.byref(n)) == 0
+    assert 64 * 8 * 4 * 4 * (2 + 128) * 4 <= n.value < 64 * 8 * 8 * 4 * (2 + 128) * 4
     assert lib.vd_attn_workspace_size(h, -1, 1, 1, ctypes.byref(n)) == -1
     assert lib.vd_pool_bytes(h, 10, ctypes.byref(n)) == 0
     assert n.value == 10 * 8 * 16 * 128 * 2
