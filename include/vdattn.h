@@ -166,6 +166,25 @@ int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len
 int vd_attn_forward(const vd_attn* h, const vd_attn_batch* batch, void* out, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
 
+/* vd_attn_forward without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same launches, same output bits; the
+ * workspace is the library's own static device array of
+ * VD_NOALLOC_SCRATCH_BYTES (128 MiB), one on every device the library runs
+ * on, held until the process ends.  A call whose vd_attn_workspace_size
+ * exceeds it returns VD_ERR_WORKSPACE before any launch (e.g. 64 requests of
+ * up to 4,096 keys need 4 MB; 8 of up to 131,072 keys 17 MB; a call with prefill
+ * rows or 4-token verify rows of a group of 8 query heads needs 32 partial
+ * states per (request, KV head, 1024-key split): 256 such requests of up to
+ * 2,560 keys 102 MB).  It allocates nothing and calls no allocating routine.
+ * Every call on one device uses that device's one array, which keeps the last
+ * call's contents (no call reads what it did not write first): calls that may
+ * overlap on one device -- other streams, other threads -- race, and the
+ * caller must order them; calls on one stream are ordered by the stream. */
+#define VD_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int vd_attn_forward_noalloc(const vd_attn* h, const vd_attn_batch* batch, void* out,
+                            hipStream_t stream);
+
 /* The four phases vd_attn_forward runs, in this order, for callers that time
  * or schedule them separately (same batch, same output, same stream, same
  * workspace; their composition is bit-identical to vd_attn_forward):

@@ -2221,6 +2221,27 @@ int run_chunks(const Params& P, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent
   return launched();
 }
 
+// The workspace of vd_attn_forward_noalloc, for callers that cannot allocate:
+// the library's own device array, one copy on every device the library runs
+// on, held until the process ends.  On the host, `scratch` names a stand-in,
+// not device memory: host code uses only the address scratch_address()
+// obtains for the current device.
+static_assert(VD_NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size");
+static __device__ __align__(256) unsigned char scratch[VD_NOALLOC_SCRATCH_BYTES];
+
+// The current device's copy of `scratch` (hipGetSymbolAddress with the device
+// current, once per device), or nullptr when it cannot be had.
+void* scratch_address() {
+  static std::atomic<void*> addr[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = addr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+  addr[dev].store(p, std::memory_order_release);
+  return p;
+}
+
 bool ws_ok(const vd_attn* h, const vd_attn_batch* b, const void* ws, size_t bytes) {
   return ws && bytes >= ws_layout(h, b->num_seqs, b->max_q_len, b->max_context_len).total;
 }
@@ -2364,6 +2385,19 @@ int vd_attn_forward(const vd_attn* h, const vd_attn_batch* b, void* out, void* w
   rc = vd_attn_forward_chunks(h, b, out, workspace, workspace_bytes, stream);
   if (rc != VD_OK) return rc;
   return vd_attn_forward_merge(h, b, out, workspace, workspace_bytes, stream);
+}
+
+int vd_attn_forward_noalloc(const vd_attn* h, const vd_attn_batch* b, void* out,
+                            hipStream_t stream) {
+  int rc = check_batch(h, b);
+  if (rc != VD_OK || b->num_seqs == 0 || b->total_q_tokens == 0) return rc;
+  if ((rc = check_out_ws(out, true, nullptr)) != VD_OK) return rc;
+  if (ws_layout(h, b->num_seqs, b->max_q_len, b->max_context_len).total > VD_NOALLOC_SCRATCH_BYTES)
+    return VD_ERR_WORKSPACE;
+  void* ws = scratch_address();
+  if (!ws) return VD_ERR_LAUNCH;
+  // the same phases as vd_attn_forward; nothing in them allocates
+  return vd_attn_forward(h, b, out, ws, VD_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int vd_attn_validate(const vd_attn* h, const vd_attn_batch* b, int32_t* status,

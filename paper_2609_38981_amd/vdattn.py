@@ -26,6 +26,7 @@ HEADER = os.path.join(ROOT, "include", "vdattn.h")
 VD_OK = 0
 VD_ABI_VERSION = 4
 VD_DTYPE_BF16 = 1
+NOALLOC_SCRATCH_BYTES = 128 << 20  # VD_NOALLOC_SCRATCH_BYTES
 TILE_KEYS = 64
 SPLIT_KEYS = 1024
 PAGE_SIZE = 16
@@ -73,6 +74,7 @@ def load_library(path: str = LIB_PATH):
         "vd_attn_destroy": (None, [P]),
         "vd_attn_workspace_size": (ctypes.c_int, [P, I32, I32, I32, ctypes.POINTER(SZ)]),
         "vd_attn_forward": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
+        "vd_attn_forward_noalloc": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P]),
         "vd_attn_forward_plan": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, SZ, P]),
         "vd_attn_forward_splits": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
         "vd_attn_forward_chunks": (ctypes.c_int, [P, ctypes.POINTER(_Batch), P, P, SZ, P]),
@@ -260,6 +262,16 @@ class VdAttn:
         ws = self._ws(b, workspace)
         _check(self.lib.vd_attn_forward(self._h, ctypes.byref(cb), _ptr(out), _ptr(ws), ws.numel(),
                                         _stream(stream)), "vd_attn_forward")
+        return out
+
+    def forward_noalloc(self, b: Batch, out: torch.Tensor, stream=None) -> torch.Tensor:
+        """vd_attn_forward_noalloc: the call with the library's own static
+        scratch as its workspace (the C call allocates nothing); ``out`` is
+        the caller's."""
+        cb = self._batch(b)
+        out = self._out(b, out)
+        _check(self.lib.vd_attn_forward_noalloc(self._h, ctypes.byref(cb), _ptr(out),
+                                                _stream(stream)), "vd_attn_forward_noalloc")
         return out
 
     def forward_plan(self, b: Batch, workspace, stream=None):

@@ -184,3 +184,33 @@ def test_forward_rejects_misaligned_pointers(lib):
         kn, vn, sm, kp, vp = args
         assert lib.vd_kv_write(h, kn, vn, sm, 3, kp, vp, 4, None) == -1, args
     lib.vd_attn_destroy(h)
+
+
+def test_noalloc_host_checks(lib):
+    """vd_attn_forward_noalloc: the checks of vd_attn_forward, and a call whose
+    workspace would exceed the library's static scratch is refused with
+    VD_ERR_WORKSPACE -- all before any device call."""
+    rc, h = _create(lib)
+    fake = 0x10000
+    limit = V.NOALLOC_SCRATCH_BYTES
+    n = ctypes.c_size_t()
+    # the workloads of the benchmark that fit, and the one that does not
+    for B, q, ctx, fits in [(64, 1, 4096, True), (8, 1, 131072, True), (256, 4, 2560, True),
+                            (128, 512, 8704, False)]:
+        hq = 64 if q == 4 else 32
+        rc2, h2 = _create(lib, num_q_heads=hq)
+        assert lib.vd_attn_workspace_size(h2, B, q, ctx, ctypes.byref(n)) == 0
+        assert (n.value <= limit) == fits, (B, q, ctx, n.value)
+        lib.vd_attn_destroy(h2)
+    big = V._Batch(128, 128 * 512, fake, fake, fake, fake, 600, fake, fake, 4, 512, 8704, None,
+                   None, 0, None)
+    assert lib.vd_attn_forward_noalloc(h, ctypes.byref(big), fake, None) == -3
+    b = V._Batch(1, 1, fake, fake, fake, fake, 1, fake, fake, 4, 1, 16, None, None, 0, None)
+    assert lib.vd_attn_forward_noalloc(h, ctypes.byref(b), None, None) == -1        # no output
+    assert lib.vd_attn_forward_noalloc(h, ctypes.byref(b), fake + 8, None) == -1    # misaligned
+    b.q = fake + 2
+    assert lib.vd_attn_forward_noalloc(h, ctypes.byref(b), fake, None) == -1
+    e = V._Batch(0, 0, None, None, None, None, 0, None, None, 0, 0, 0, None, None, 0, None)
+    assert lib.vd_attn_forward_noalloc(h, ctypes.byref(e), None, None) == 0        # nothing to do
+    assert lib.vd_attn_forward_noalloc(None, ctypes.byref(b), fake, None) == -1
+    lib.vd_attn_destroy(h)

@@ -1,0 +1,67 @@
+"""The allocation-free entry point (vd_attn_forward_noalloc, for callers that
+cannot allocate device memory): through the C ABI, its output equals
+vd_attn_forward's with a caller workspace bit for bit, on consecutive calls
+that reuse the library's static scratch, each later call smaller than the one
+before -- a full-size 8B decode batch, then a mixed batch whose new tokens
+are written by the plan launch, then a prefix-shared verify batch (the
+shared-prefix pass) -- and the rows are within tolerance of the oracle."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_38981_amd import staging as S
+from paper_2609_38981_amd import vdattn as V
+from paper_2609_38981_amd import workloads as W
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    U.require_gpu()
+
+
+def run_both(call, append=False):
+    """(vd_attn_forward with a workspace, vd_attn_forward_noalloc) output bits."""
+    attn = U.handle(call.shape)
+    dc = S.to_device(attn, call, poison=True, append=append)
+    b = dc.batch
+    need = attn.workspace_size(call.num_seqs, b.max_q_len, b.max_context_len)
+    assert need <= V.NOALLOC_SCRATCH_BYTES, need
+    outs = []
+    for noalloc in (False, True):
+        if append:
+            # the call writes its new tokens into the pool: restore the pool
+            # so that both runs read the same keys
+            S.fill_pool(attn, call, b.k_pool, b.v_pool)
+        out = torch.empty_like(b.q)
+        out.view(torch.int16).fill_(U.FILL)
+        if noalloc:
+            attn.forward_noalloc(b, out)
+        else:
+            ws = attn.new_workspace(call.num_seqs, b.max_q_len, b.max_context_len)
+            ws.view(torch.int8).fill_(-1)
+            attn.forward(b, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        outs.append(S.bits_of(out))
+    return outs
+
+
+def test_noalloc_equals_forward_on_consecutive_calls():
+    calls = [
+        ("8B decode, 64 requests", W.config2(), False),
+        ("mixed, new tokens handed over", W.config3(num_prefill=2, chunk=96, max_off=900,
+                                                    num_decode=10, dec_lo=60, dec_hi=1500), True),
+        ("70B prefix-shared verify", W.config5(num_req=8, prefix=2048, suf_lo=30, suf_hi=200),
+         False),
+    ]
+    for name, call, append in calls:
+        U.say("noalloc: %s (%d requests, %d rows)" % (name, call.num_seqs, call.total_q_tokens))
+        ref, got = run_both(call, append=append)
+        rows = U.by_position(call, ref)
+        U.assert_same_bits(rows, U.by_position(call, got), min_common=call.total_q_tokens)
+        sample = sorted({0, call.total_q_tokens // 2, call.total_q_tokens - 1})
+        U.say("  bit-identical; vs oracle: %s" % U.parity(call, got, rows=sample))
