@@ -444,12 +444,13 @@ def main():
                     "avg_ms": round(k_ms, 5), "timed_launches": launches,
                     "algorithmic_flop": int(chunk_flops)}
         # K+V of the visible keys, Q, the page-table entries read; and when the
-        # split items write the call's new tokens themselves (every row on the
-        # split path, at most 16 query rows per request, at most 256 requests),
-        # the new K+V rows read from k_new / v_new and written to the pool
+        # split launch writes the call's new tokens (at most 256 requests, and
+        # at most 16 query rows per split-path request: groups of two or more
+        # query heads, or max_q_len <= 16), every query row's K+V read from
+        # k_new / v_new and written to the pool
         alg = split_bytes + sum(r.s for r in split_reqs) * hq * D * 2 + \
             sum(-(-r.n // P) - call.first_key(i) // P for i, r in zip(split_idx, split_reqs)) * 4
-        if len(split_reqs) == call.num_seqs <= 256 and call.max_q_len <= 16:
+        if call.num_seqs <= 256 and (G >= 2 or call.max_q_len <= 16):
             alg += 2 * T * hkv * D * 2 * 2
         ach = alg / (k_ms * 1e-3) / 1e9
         # with the shared_pages hint the library's shared-prefix pass runs

@@ -189,18 +189,21 @@ int vd_attn_forward_noalloc(const vd_attn* h, const vd_attn_batch* batch, void* 
  * or schedule them separately (same batch, same output, same stream, same
  * workspace; their composition is bit-identical to vd_attn_forward):
  *   plan:   only for calls with more than 256 requests, with k_new / v_new
- *           that the split items do not write (some s_r * (Hq / Hkv) > 32 or
- *           s_r > 16, by the hints), or with the shared_pages hint; otherwise
- *           it launches nothing.  Writes k_new / v_new into the pool and,
- *           reading the per-request lengths and page tables on the device, the
- *           work lists of the split and shared-prefix phases into the
- *           workspace (no device-to-host synchronisation);
+ *           that the split launch does not write (Hq / Hkv = 1 and
+ *           max_q_len > 16), or with the shared_pages hint; otherwise it
+ *           launches nothing.  Writes k_new / v_new into the pool (when the
+ *           split launch does not) and, reading the per-request lengths and
+ *           page tables on the device, the work lists of the split and
+ *           shared-prefix phases into the workspace (no device-to-host
+ *           synchronisation);
  *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
  *           per (request, KV head, 1024-key split, 16 query-head rows), after
  *           the shared-prefix items (shared_pages hint) -- one per (group, KV
  *           head, 128 query-head rows of its members, shared split).  Without
  *           a plan launch, every workgroup derives its items from the lengths
- *           and the items write the call's new tokens themselves.  A request
+ *           and the call's new tokens are written by this launch: the items
+ *           write their own requests' rows, and further workgroups, after
+ *           the items', those of the requests of the chunks phase.  A request
  *           with one split writes its output rows directly; otherwise each
  *           item writes a partial state;
  *   chunks: rows of requests with s_r * (Hq / Hkv) > 32 -- one work item per

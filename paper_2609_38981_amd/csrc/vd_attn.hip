@@ -76,10 +76,12 @@ struct Params {
   float c;  // softmax scale * log2(e), rounded once to fp32 on the host
   // optional K/V of the call's query rows ([T, Hkv, D]), written into the pool
   // before attention reads it: by the plan launch, or (fuse_write) by the
-  // split items themselves
+  // split launch -- the split items write the rows of their own requests, and
+  // the launch's last append_wgs workgroups (0: none) those of the chunk-path
+  // requests, which the chunk launch reads after it
   const uint16_t* knew;
   const uint16_t* vnew;
-  int fuse_write;
+  int fuse_write, append_wgs;
   // the split workgroups derive their items from the lengths (no plan launch)
   int inwave;
   float* lse;  // optional [T, Hq] log-sum-exp output
@@ -1245,6 +1247,133 @@ __device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& 
          qt < (ncols + kChunkCols - 1) / kChunkCols;
 }
 
+// The new tokens of the chunk-path requests, written by the split launch's
+// last workgroups (calls of at most kInWaveMaxSeqs requests).  Unit u is
+// (request, run of its new positions n - s .. n - 1 within one page, KV
+// head): units are listed request by request (chunk-path requests only), runs
+// ascending, KV heads fastest.  One wavefront per unit, all of its loads in
+// flight together: lane l loads the 16-byte pieces q = l, l + 64, ... (row
+// q / (D / 8), d from 8 (q % (D / 8))) of the run's K and V rows; K pieces are
+// stored as they are; V rows go to the wavefront's LDS rows `lds` (16 x D
+// bf16), from which a whole page is stored as 16-byte pieces of its V block
+// (2 d x 4 slots each) and a partial run value by value.  Returns false when u
+// is past the call's units.  A page id outside the pool is not written.
+template <int D>
+__device__ __forceinline__ bool append_unit(const Params& P, int u, uint16_t* lds) {
+  constexpr int C = kInWaveChunks;
+  constexpr int PPR = D / 8;                 // 16-byte pieces per row
+  constexpr int NQ = kPage * PPR / 64;       // pieces per lane for a whole page
+  const int lane = __lane_id();
+  int cq0[C], cq1[C], cn[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int rr = min(64 * c + lane, P.num_seqs - 1);
+    cq0[c] = P.cu[rr];
+    cq1[c] = P.cu[rr + 1];
+    cn[c] = P.ctx[rr];
+  }
+  int cnt[C], incl[C];
+  int total = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    cnt[c] = 0;
+    incl[c] = 0;
+    if (64 * c >= P.num_seqs) continue;
+    if (64 * c + lane < P.num_seqs) {
+      const Req Rl = make_req(P, cq0[c], cq1[c], cn[c]);
+      if (Rl.valid && Rl.s * P.G > P.split_cols)
+        cnt[c] = ((Rl.n - 1) / kPage - (Rl.n - Rl.s) / kPage + 1) * P.hkv;
+    }
+    incl[c] = wave_scan_dpp(cnt[c]);
+    total += __builtin_amdgcn_readlane(incl[c], 63);
+  }
+  if (u >= total) return false;
+  int j = -1, cj = 0, rem = 0, base = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int tot = __builtin_amdgcn_readlane(incl[c], 63);
+    if (j < 0 && u < base + tot) {
+      j = __builtin_ctzll(__ballot(incl[c] > u - base));
+      cj = c;
+      rem = u - base - __builtin_amdgcn_readlane(incl[c] - cnt[c], j);
+    }
+    base += tot;
+  }
+  int q0 = 0, q1 = 0, n = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+    if (c == cj) {
+      q0 = __builtin_amdgcn_readlane(cq0[c], j);
+      q1 = __builtin_amdgcn_readlane(cq1[c], j);
+      n = __builtin_amdgcn_readlane(cn[c], j);
+    }
+  const int r = uni(64 * cj + j);
+  const Req R = make_req(P, q0, q1, n);
+  const int run = uni(rem / P.hkv), h = uni(rem % P.hkv);
+  const int p0 = R.n - R.s;
+  const int lp = p0 / kPage + run;             // the run's logical page
+  const int start = max(p0, lp * kPage), end = min(R.n, lp * kPage + kPage);
+  if (!R.valid || r >= P.num_seqs || start >= end) return true;
+  const int rows = end - start, slot0 = start % kPage;
+  const int32_t page = P.pt[(int64_t)r * P.pt_stride + lp];
+  const int64_t t0 = R.q0 + (start - p0);
+  u16x8 kv[NQ], vv[NQ];
+#pragma unroll
+  for (int x = 0; x < NQ; ++x) {
+    const int q = 64 * x + lane, i = q / PPR, dc = q % PPR;
+    const int64_t src = ((t0 + i) * P.hkv + h) * D + 8 * dc;
+    kv[x] = i < rows ? *reinterpret_cast<const u16x8*>(P.knew + src) : zero8();
+    vv[x] = i < rows ? *reinterpret_cast<const u16x8*>(P.vnew + src) : zero8();
+  }
+#pragma unroll
+  for (int x = 0; x < NQ; ++x) {
+    const int q = 64 * x + lane;
+    *reinterpret_cast<u16x8*>(lds + (q / PPR) * D + 8 * (q % PPR)) = vv[x];
+  }
+  lds_barrier();  // the workgroup is this one wavefront
+  if (page < 0 || page >= P.num_pages) return true;
+  const int64_t blk = ((int64_t)page * P.hkv + h) * (kPage * D);
+  uint16_t* kpool = const_cast<uint16_t*>(P.kpool);
+  uint16_t* vpool = const_cast<uint16_t*>(P.vpool);
+  // K block: element (slot, d) at ((d / 8) * 16 + slot) * 8 + d % 8
+#pragma unroll
+  for (int x = 0; x < NQ; ++x) {
+    const int q = 64 * x + lane, i = q / PPR, dc = q % PPR;
+    if (i < rows) *reinterpret_cast<u16x8*>(kpool + blk + ((int64_t)dc * kPage + slot0 + i) * 8) = kv[x];
+  }
+  // V block: element (slot, d) at ((d / 16) * 4 + slot / 4) * 64 + (d % 16) * 4 + slot % 4;
+  // its 16-byte piece e holds d = 2 (e % 8) + 16 (e / 32) and d + 1 for the
+  // slots 4 ((e / 8) % 4) .. + 3
+#pragma unroll
+  for (int x = 0; x < NQ; ++x) {
+    const int e = 64 * x + lane;
+    const int d = 16 * (e / 32) + 2 * (e % 8), sg = (e / 8) % 4;
+    uint32_t w[4];
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+      const int i = 4 * sg + y - slot0;  // the slot's row of the run (rows past it hold zeros)
+      w[y] = i >= 0 ? *reinterpret_cast<const uint32_t*>(lds + i * D + d) : 0u;
+    }
+    uint16_t* dst = vpool + blk + 8 * e;
+    if (rows == kPage) {
+      const u16x8 o = {(uint16_t)w[0], (uint16_t)w[1], (uint16_t)w[2], (uint16_t)w[3],
+                       (uint16_t)(w[0] >> 16), (uint16_t)(w[1] >> 16), (uint16_t)(w[2] >> 16),
+                       (uint16_t)(w[3] >> 16)};
+      *reinterpret_cast<u16x8*>(dst) = o;
+    } else {
+#pragma unroll
+      for (int y = 0; y < 4; ++y) {
+        const int slot = 4 * sg + y;
+        if (slot >= slot0 && slot < slot0 + rows) {
+          dst[y] = (uint16_t)w[y];
+          dst[4 + y] = (uint16_t)(w[y] >> 16);
+        }
+      }
+    }
+  }
+  return true;
+}
+
 // One wavefront per workgroup, 16 columns per item (two wavefronts per SIMD
 // at head_dim 128): a finished item frees its slot at once, which keeps the
 // end of the launch short when item durations vary.  The grid is capped at
@@ -1255,9 +1384,20 @@ __device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& 
 template <int D, bool WIN, bool NT>
 __global__ __launch_bounds__(64) void split_kernel(Params P) {
   __shared__ __attribute__((aligned(16))) uint16_t vlds[kMaxNewRows * D];
+  // The last append_wgs workgroups write the new tokens of the chunk-path
+  // requests (units b - grid, b - grid + append_wgs, ...): dispatched after
+  // every split workgroup, they run in the launch's tail, when the shortest
+  // items leave the memory system room.  (Dispatched first, they delayed the
+  // split items: 35 us more for the 8B mixed batch, against 11 us.)
+  const int grid = (int)gridDim.x - P.append_wgs;
+  if ((int)blockIdx.x >= grid) {
+    for (int u = blockIdx.x - grid; append_unit<D>(P, u, vlds); u += P.append_wgs) {
+    }
+    return;
+  }
   const int64_t slots = split_slots(P);  // work-list length
   int per_xcd = 0;
-  for (int vb = blockIdx.x;; vb += gridDim.x) {
+  for (int vb = blockIdx.x;; vb += grid) {
     int r, g, k, half;
     Req R;
     if (P.inwave) {
@@ -1290,7 +1430,7 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
       R.valid = true;
     }
     split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds, half);
-    if (P.inwave && ((vb + (int)gridDim.x) >> P.xcd_shift) >= per_xcd) return;  // no further slot holds an item
+    if (P.inwave && ((vb + grid) >> P.xcd_shift) >= per_xcd) return;  // no further slot holds an item
   }
 }
 
@@ -2031,15 +2171,21 @@ bool needs_chunks(const vd_attn* h, const vd_attn_batch* b) {
   return (int64_t)b->max_q_len * h->group > kSplitCols;
 }
 
+// The same from a call's parameters.
+bool needs_chunks_params(const Params& P) { return (int64_t)P.max_q * P.G > kSplitCols; }
+
 // Calls of at most kInWaveMaxSeqs requests need no work lists: the split and
 // chunk workgroups derive their items from the lengths.
 bool plans_inwave(const vd_attn_batch* b) { return b->num_seqs <= kInWaveMaxSeqs; }
 
-// The split items write the call's new tokens themselves when every row is on
-// the split path, with at most kMaxNewRows query rows per request.
+// The split launch writes the call's new tokens when its workgroups plan for
+// themselves and no split-path request has more than kMaxNewRows query rows
+// (s * G <= 32 keeps s <= 16 for groups of two or more query heads): the
+// split items those of their own requests, the launch's last workgroups
+// those of the chunk-path requests.
 bool fuses_write(const vd_attn* h, const vd_attn_batch* b) {
-  return b->k_new != nullptr && plans_inwave(b) && !needs_chunks(h, b) &&
-         b->max_q_len <= kMaxNewRows;
+  return b->k_new != nullptr && plans_inwave(b) &&
+         (h->group >= 2 || b->max_q_len <= kMaxNewRows);
 }
 
 // The shared-prefix pass runs for calls with the shared_pages hint: at most
@@ -2100,6 +2246,7 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.inwave = plans_inwave(b);
   P.lse = b->lse;
   P.fuse_write = fuses_write(h, b);
+  P.append_wgs = 0;  // set by the split launch
   P.casc = cascades(h, b);
   P.casc_hdr = reinterpret_cast<int32_t*>(w + L.casc_hdr);
   P.casc_seq = reinterpret_cast<int32_t*>(w + L.casc_seq);
@@ -2131,8 +2278,9 @@ auto split_kernel_for(const Params& P) {
 }
 
 template <int D>
-int run_splits(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e0 = nullptr,
+int run_splits(const Params& P0, bool stream_kv, hipStream_t s, hipEvent_t e0 = nullptr,
                hipEvent_t e1 = nullptr) {
+  Params P = P0;
   // upper bound of the split items (the work-list length); a workgroup stops
   // at its first slot past the call's items.  Workgroups that plan for
   // themselves take XCD-contiguous ranges of the items.
@@ -2142,7 +2290,17 @@ int run_splits(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e0 = n
   // compute unit, two wavefronts each); a multiple of the dies
   const Geometry geo = device_geometry();
   const int64_t cap = 16 * (int64_t)geo.cus;
-  const dim3 grid((unsigned)((std::min(items, cap) + geo.xcds - 1) / geo.xcds * geo.xcds)), block(64);
+  const int64_t split_wgs = (std::min(items, cap) + geo.xcds - 1) / geo.xcds * geo.xcds;
+  // the chunk-path requests' new tokens: a workgroup per unit up to the cap
+  // (an upper bound of the units: every request's page runs number at most
+  // s / 16 + 2, times the KV heads), dispatched after the split workgroups
+  int64_t append = 0;
+  if (P.fuse_write && needs_chunks_params(P)) {
+    const int64_t units = ((P.T + kPage - 1) / kPage + 2 * (int64_t)P.num_seqs) * P.hkv;
+    append = (std::min(units, cap) + geo.xcds - 1) / geo.xcds * geo.xcds;
+  }
+  P.append_wgs = (int)append;
+  const dim3 grid((unsigned)(split_wgs + append)), block(64);
   const auto kern = stream_kv ? split_kernel_for<D, true>(P) : split_kernel_for<D, false>(P);
   hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, P);
   return launched();

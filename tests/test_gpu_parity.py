@@ -184,3 +184,37 @@ def test_append_then_attend(name):
     b = U.gpu_run(call)
     assert np.array_equal(a, b)
     U.say("  append %s: %s" % (name, U.parity(call, a)))
+
+
+APPEND_LENS = [(300, 100), (97, 40), (1500, 1), (700, 4), (64, 64), (1100, 33), (17, 17)]
+
+
+@pytest.mark.parametrize("shape", [W.TINY, W.LLAMA8B, W.LLAMA70B, W.Shape(8, 8, 64)],
+                         ids=["g2_d64", "g4_d128", "g8_d128", "g1_d64"])
+def test_append_writes_the_pool_like_kv_write(shape):
+    """A call handed its new tokens (k_new / v_new) leaves the pools bit for
+    bit as vd_kv_write of every token would: runs of new positions that start
+    and end inside pages, rows on the split path (written by the split items)
+    and on the chunk path (written by the split launch's append workgroups, or
+    by the plan launch when a split-path request may hold more than 16 rows);
+    the slots of other positions keep their NaN fill.  The outputs equal those
+    of the call whose tokens were written beforehand."""
+    prompts = [W.make_prompt(shape, n, 16, i, q_window=s) for i, (n, s) in enumerate(APPEND_LENS)]
+    call = W.place(shape, prompts, [W.Req(i, n, s) for i, (n, s) in enumerate(APPEND_LENS)],
+                   W.rng_for(16, 4))
+    attn = U.handle(shape)
+    outs, pools = [], []
+    for append in (True, False):
+        dc = S.to_device(attn, call, poison=True, append=append)
+        out = torch.empty_like(dc.batch.q)
+        out.view(torch.int16).fill_(U.FILL)
+        ws = attn.new_workspace(call.num_seqs, dc.batch.max_q_len, dc.batch.max_context_len)
+        attn.forward(dc.batch, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        outs.append(S.bits_of(out))
+        pools.append((S.bits_of(dc.batch.k_pool), S.bits_of(dc.batch.v_pool)))
+    assert np.array_equal(pools[0][0], pools[1][0]), "K pool differs from vd_kv_write's"
+    assert np.array_equal(pools[0][1], pools[1][1]), "V pool differs from vd_kv_write's"
+    U.assert_same_bits(U.by_position(call, outs[0]), U.by_position(call, outs[1]),
+                       min_common=call.total_q_tokens)
+    U.say("  append %s: %s" % (shape, U.parity(call, outs[0])))
