@@ -28,6 +28,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "vd_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# another build of the same source, e.g. with sanitizers (oracle/sanitize.py)
+_OVERRIDE = os.environ.get("VDO_ORACLE_LIB")
 _lock = threading.Lock()
 _lib = None
 
@@ -77,8 +79,11 @@ def _load():
     global _lib
     with _lock:
         if _lib is None:
-            build(force=False)
-            _lib = bind(_LIB)
+            if _OVERRIDE:
+                _lib = bind(_OVERRIDE)
+            else:
+                build(force=False)
+                _lib = bind(_LIB)
     return _lib
 
 

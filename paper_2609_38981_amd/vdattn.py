@@ -20,7 +20,9 @@ import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-LIB_PATH = os.path.join(HERE, "libvdattn.so")
+# the in-tree build, or another build of the same sources (VDATTN_LIB: e.g. the
+# host code built with sanitizers, oracle/sanitize.py)
+LIB_PATH = os.environ.get("VDATTN_LIB") or os.path.join(HERE, "libvdattn.so")
 HEADER = os.path.join(ROOT, "include", "vdattn.h")
 
 VD_OK = 0
