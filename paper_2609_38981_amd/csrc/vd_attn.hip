@@ -1677,22 +1677,49 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int kt_first = window_lo(R.n - R.s + c0 / P.G, window) / kTileKeys;
   // this wavefront's smallest window start (its first valid column)
   const int wave_lo = window_lo(R.n - R.s + min(c0 + wave * 32, cend - 1) / P.G, window);
+  const int npages = (R.n + kPage - 1) / kPage;
+  // whether every page id of the request's table row lies in the pool: then
+  // a tile is full (needs no masking) when it lies below n, without looking
+  // its pages up again
+  bool bad = false;
+  for (int e = lane; e < npages; e += 64) {
+    const int32_t pg = ptrow[e];
+    bad = bad || pg < 0 || pg >= P.num_pages;
+  }
+  const bool pages_ok = !__any(bad);
+  // The page blocks of tile kt (-1: past the request's pages or outside the
+  // pool); a tile below the request's last page takes its 4 table entries in
+  // one scalar load.
+  auto tile_blocks = [&](int kt, int64_t (&pb)[kPagesPerTile]) {
+    const int lp0 = kt * kPagesPerTile;
+    if (lp0 + kPagesPerTile <= npages) {
+      typedef __attribute__((address_space(4))) const int32_t const_i32;
+      const const_i32* e = (const const_i32*)(ptrow + lp0);
+      const int32_t pg[kPagesPerTile] = {e[0], e[1], e[2], e[3]};
+#pragma unroll
+      for (int b = 0; b < kPagesPerTile; ++b)
+        pb[b] = (pg[b] < 0 || pg[b] >= P.num_pages) ? -1 : (int64_t)pg[b] * P.hkv + g;
+    } else {
+#pragma unroll
+      for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, lp0 + b, R.n, g);
+    }
+  };
   // Issues this wavefront's WCH direct loads of tile kt into stage buf: copy
-  // q = wave * WCH + w moves 1 KB of page block q / (BLK / 512).
+  // q = wave * WCH + w moves 1 KB of page block q / (BLK / 512); a wavefront's
+  // copies cover whole page blocks, whose 1 KB parts share one M0 setting.
+  constexpr int SUBS = BLK / 512;  // 1 KB copies per page block
+  static_assert(WCH % SUBS == 0, "whole page blocks per wavefront");
   auto fetch = [&](int kt, int buf) {
     int64_t pb[kPagesPerTile];
+    tile_blocks(kt, pb);
 #pragma unroll
-    for (int b = 0; b < kPagesPerTile; ++b) pb[b] = page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g);
-#pragma unroll
-    for (int w = 0; w < WCH; ++w) {
-      const int q = wave * WCH + w;
-      const int blk = q / (BLK / 512), sub = q % (BLK / 512);
+    for (int w = 0; w < WCH; w += SUBS) {
+      const int blk = (wave * WCH + w) / SUBS;
       const int b = blk % kPagesPerTile;
       const int64_t pbb = pb[b] < 0 ? 0 : pb[b];
-      const uint16_t* src =
-          block_ptr<D>(blk < kPagesPerTile ? P.kpool : P.vpool, pbb) + 512 * sub + 8 * lane;
-      const uint32_t dst = (uint32_t)(uintptr_t)(lds + (buf * NBLK + blk) * BLK + 512 * sub);
-      lds_dma16(src, uni((int)dst));
+      const uint16_t* src = block_ptr<D>(blk < kPagesPerTile ? P.kpool : P.vpool, pbb) + 8 * lane;
+      const uint32_t dst = (uint32_t)(uintptr_t)(lds + (buf * NBLK + blk) * BLK);
+      lds_dma16_run<SUBS>(src, uni((int)dst));
     }
   };
   // Zeroes, in stage buf, the K rows and V entries of keys >= n or of
@@ -1723,6 +1750,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   };
   auto tile_is_full = [&](int kt) {
     if ((kt + 1) * kTileKeys > R.n) return false;
+    if (pages_ok) return true;
 #pragma unroll
     for (int b = 0; b < kPagesPerTile; ++b)
       if (page_block(P, ptrow, kt * kPagesPerTile + b, R.n, g) < 0) return false;
@@ -1929,19 +1957,21 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
   auto tile_pages = [&](int kt) {
     return *reinterpret_cast<const int4*>(spid + (kt - kt0) * kPagesPerTile);
   };
+  // a wavefront's copies cover whole page blocks, whose 1 KB parts share one
+  // M0 setting
+  constexpr int SUBS = BLK / 512;
+  static_assert(WCH % SUBS == 0, "whole page blocks per wavefront");
   auto fetch = [&](int kt, int buf) {
     const int4 pg = tile_pages(kt);
     const int pages[kPagesPerTile] = {pg.x, pg.y, pg.z, pg.w};
 #pragma unroll
-    for (int w = 0; w < WCH; ++w) {
-      const int q = wave * WCH + w;
-      const int blk = q / (BLK / 512), sub = q % (BLK / 512);
+    for (int w = 0; w < WCH; w += SUBS) {
+      const int blk = (wave * WCH + w) / SUBS;
       const int page = uni(pages[blk % kPagesPerTile]);
       const int64_t pbb = page < 0 ? 0 : (int64_t)page * P.hkv + g;
-      const uint16_t* src =
-          block_ptr<D>(blk < kPagesPerTile ? P.kpool : P.vpool, pbb) + 512 * sub + 8 * lane;
-      const uint32_t dst = (uint32_t)(uintptr_t)(lds + (buf * NBLK + blk) * BLK + 512 * sub);
-      lds_dma16(src, uni((int)dst));
+      const uint16_t* src = block_ptr<D>(blk < kPagesPerTile ? P.kpool : P.vpool, pbb) + 8 * lane;
+      const uint32_t dst = (uint32_t)(uintptr_t)(lds + (buf * NBLK + blk) * BLK);
+      lds_dma16_run<SUBS>(src, uni((int)dst));
     }
   };
   // a page id outside the pool reads as zeros, as on the split path

@@ -37,6 +37,40 @@ __device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0val) {
       : "memory");
 }
 
+// N direct global-to-LDS copies of 1 KB (N = 2 or 4) with one M0 setting:
+// copy i moves lane l's 16 bytes from src + 1024 i to LDS byte address
+// m0val + 1024 i + 16 l (the instruction's immediate offset moves both the
+// global and the LDS address).  M0 is saved and restored, as in lds_dma16.
+template <int N>
+__device__ __forceinline__ void lds_dma16_run(const void* src, uint32_t m0val) {
+  static_assert(N == 2 || N == 4, "copies per M0 setting");
+  uint32_t saved;
+  if constexpr (N == 4)
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "global_load_lds_dwordx4 %1, off offset:1024\n\t"
+        "global_load_lds_dwordx4 %1, off offset:2048\n\t"
+        "global_load_lds_dwordx4 %1, off offset:3072\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(src), "s"(m0val)
+        : "memory");
+  else
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "global_load_lds_dwordx4 %1, off offset:1024\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(src), "s"(m0val)
+        : "memory");
+}
+
 // 8-byte LDS read issued as its own ds_read_b64.  Volatile, so that the
 // compiler does not pair it with a neighbour at another offset into one
 // two-address read: the two halves of a matrix operand come from two page
