@@ -175,9 +175,14 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
   TileWeights w;
   w.h = !MASKED || (j0 <= p && (!WIN || j0 + kTileKeys - 1 >= lo));  // any visible key
   w.m_new = fmax_(st.m, mx);
-  // A column with no visible key keeps its state (tile_commit), and its
-  // operands are zeroed so that nothing non-finite enters the matrix core.
-  w.alpha = w.h ? ex2(st.m - w.m_new) : 0.0f;
+  // A column with no visible key keeps its state: its weights are all +0
+  // (every lam is false), so with alpha = 1 the P.V step adds only zero
+  // products to U * 1 = U, which the matrix core returns bit for bit (probe on
+  // gfx950: every finite accumulator, denormals included, except -0, which
+  // comes back +0 -- and U is never -0: it starts at +0 and only non-negative
+  // weights enter it); z * 1 + 0 = z, and tile_commit keeps (m, z).  (m is
+  // -inf before the first visible key: ex2 of -inf - -inf would be NaN.)
+  w.alpha = w.h ? ex2(st.m - w.m_new) : 1.0f;
   float a[kPagesPerTile][4];
 #pragma unroll
   for (int b = 0; b < kPagesPerTile; ++b)
@@ -199,14 +204,17 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
 }
 
 // P.V for d-block m: U <- dot(bf16(A), V, U * alpha), keys in two 32-wide
-// halves in ascending order (v0: keys 0-31 of the tile, v1: keys 32-63).
+// halves in ascending order (v0: keys 0-31 of the tile, v1: keys 32-63).  For
+// a column without a visible key (h = 0) this is the identity step described
+// in tile_softmax: alpha = 1 and zero weights leave U as it was, so no select
+// follows the products.  V must be finite for the keys of the tile (keys past
+// n are zeroed by the kernels; the others are the cache's values).
 template <int D>
 __device__ __forceinline__ void tile_pv_block(State<D>& st, const TileWeights& w, int m,
                                               const u16x8& v0, const u16x8& v1) {
   f32x4 u = st.u[m] * w.alpha;
   u = mfma(v0, w.pf[0], u);
-  u = mfma(v1, w.pf[1], u);
-  st.u[m] = w.h ? u : st.u[m];
+  st.u[m] = mfma(v1, w.pf[1], u);
 }
 
 // (m, z) <- select(h, new, old)
