@@ -386,18 +386,19 @@ __host__ __device__ __forceinline__ int64_t split_slots(const Params& P) {
 }
 
 // Work-list entry of one split item: request, KV head, split index, the
-// request's lengths and the column half, so that a split wavefront reaches
-// its first K/V loads after a single scalar load.  r = -1 marks an unused slot.
-constexpr int kItemInts = 8;  // {r, g, k, n, q0, s, half, 0}
+// request's lengths, the column half and the request's leading splits that the
+// shared-prefix kernel computes, so that a split wavefront reaches its first
+// K/V loads after a single scalar load.  r = -1 marks an unused slot.
+constexpr int kItemInts = 8;  // {r, g, k, n, q0, s, half, pre}
 // Number of counters of the planning scan: whole splits, chunk q-tiles, and
 // the last (partial) splits by their tile count, 16 down to 1.
 constexpr int kPlanCounters = 2 + kTilesPerSplit;
 
 __device__ __forceinline__ void put_item(const Params& P, int64_t idx, int r, int g, int k,
-                                         const Req& R, int half) {
+                                         const Req& R, int half, int pre) {
   int4* e = reinterpret_cast<int4*>(P.items + idx * kItemInts);
   e[0] = int4{r, g, k, R.n};
-  e[1] = int4{R.q0, R.s, half, 0};
+  e[1] = int4{R.q0, R.s, half, pre};
 }
 
 // ---------------------------------------------------------------------------
@@ -731,11 +732,14 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
       const int kfirst = max(window_lo(R.n - R.s, P.window) / kSplitKeys, P.casc ? csq[r] : 0);
       const int nf = nfull - kfirst;  // whole splits with items
       const int h = column_halves(R, P.G);
+      const int pre = P.casc ? csq[r] : 0;
       // items (KV head, split, half), halves adjacent
       for (int idx = lane; idx < P.hkv * nf * h; idx += 64)
-        put_item(P, (int64_t)rfo + idx, r, idx / (nf * h), kfirst + idx % (nf * h) / h, R, idx % h);
+        put_item(P, (int64_t)rfo + idx, r, idx / (nf * h), kfirst + idx % (nf * h) / h, R, idx % h,
+                 pre);
       if (R.n % kSplitKeys)
-        for (int x = lane; x < P.hkv * h; x += 64) put_item(P, (int64_t)rpo + x, r, x / h, nfull, R, x % h);
+        for (int x = lane; x < P.hkv * h; x += 64)
+          put_item(P, (int64_t)rpo + x, r, x / h, nfull, R, x % h, pre);
     }
   }
   // Pass 3: slots past the list end the split workgroups' loops
@@ -911,13 +915,22 @@ __device__ __forceinline__ void apply_v_new(const Params& P, const uint16_t* lds
   }
 }
 
+// A request whose splits 0 .. pre - 1 the shared-prefix kernel computed (a
+// launch before this one) and whose last split is split pre: that split's
+// items fold the earlier partial states with their own and store the rows,
+// and the merge kernels leave the request alone.
+__device__ __forceinline__ bool folds_prefix(const Req& R, int pre) {
+  return pre >= 1 && (R.n - 1) / kSplitKeys == pre;
+}
+
 // One split item: the tiles of split k of request r, KV head g, for NA
 // column blocks of 16 query-head rows, from column 16 * NA * half.  WIN: the
 // handle has a sliding window.  vlds: LDS rows for the call's new V rows
-// (kMaxNewRows * D bf16); the item of half 0 writes them to the pool.
+// (kMaxNewRows * D bf16); the item of half 0 writes them to the pool.  pre:
+// the request's leading splits computed by the shared-prefix kernel.
 template <int D, int NA, bool WIN, bool NT>
 __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k, const Req& R,
-                                           uint16_t* vlds, int half) {
+                                           uint16_t* vlds, int half, int pre) {
   const int window = WIN ? P.window : 0;
   const int lane = __lane_id();
   const int col = lane & 15, grp = lane >> 4;
@@ -1011,6 +1024,47 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     }
     return;
   }
+  if (!WIN && k == pre && folds_prefix(R, pre)) {
+    // the left fold of the merge kernels over splits 0 .. k (every row of a
+    // member sees all of them), splits 0 .. k - 1 from the partial states,
+    // then this item's own state; the row is stored here
+#pragma unroll
+    for (int nb = 0; nb < NA; ++nb) {
+      if (pos[nb] < 0) continue;
+      const int c = cbase + nb * 16 + col;
+      const int64_t base = ((int64_t)(r * P.hkv + g) * P.ws_cols + c) * MS;
+      float M = P.ws_m[base], Z = P.ws_z[base];
+      f32x4 W[D / 16];
+#pragma unroll
+      for (int m = 0; m < D / 16; ++m)
+        W[m] = *reinterpret_cast<const f32x4*>(P.ws_u + base * D + 16 * m + 4 * grp);
+      for (int j = 1; j <= k; ++j) {
+        float mj, zj;
+        f32x4 uj[D / 16];
+        if (j < k) {
+          mj = P.ws_m[base + j];
+          zj = P.ws_z[base + j];
+#pragma unroll
+          for (int m = 0; m < D / 16; ++m)
+            uj[m] = *reinterpret_cast<const f32x4*>(P.ws_u + (base + j) * D + 16 * m + 4 * grp);
+        } else {
+          mj = st[nb].m;
+          zj = st[nb].z;
+#pragma unroll
+          for (int m = 0; m < D / 16; ++m) uj[m] = st[nb].u[m];
+        }
+        const FoldScalars f = fold_scalars(M, Z, mj, zj);
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) W[m][e] = fold_value(W[m][e], uj[m][e], f);
+        M = f.M;
+        Z = f.Z;
+      }
+      store_row<D>(P, W, M, Z, R.q0 + c / P.G, g * P.G + c % P.G);
+    }
+    return;
+  }
   // partial state of split k for every column that has a visible key in it
 #pragma unroll
   for (int nb = 0; nb < NA; ++nb) {
@@ -1042,6 +1096,7 @@ constexpr int kInWaveMaxSeqs = 64 * kInWaveChunks;
 
 struct SplitRef {
   int r, g, k, half;
+  int pre;  // the request's leading splits computed by the shared-prefix kernel
   Req R;
   int per_xcd;  // items each XCD takes (slots b with b / xcds < per_xcd hold one)
 };
@@ -1172,6 +1227,7 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
   // a whole split found above, or the request's last (partial) split
   out.k = uni(is_whole ? kj : n / kSplitKeys);
   out.half = uni(hj);
+  out.pre = uni(cc);
   // the item addresses only the request's own table row, rows and partial
   // states: check that it is one of the request's splits and halves
   return out.r < P.num_seqs && out.g < P.hkv && out.R.valid && out.R.s * P.G <= P.split_cols &&
@@ -1398,7 +1454,7 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
   const int64_t slots = split_slots(P);  // work-list length
   int per_xcd = 0;
   for (int vb = blockIdx.x;; vb += grid) {
-    int r, g, k, half;
+    int r, g, k, half, pre;
     Req R;
     if (P.inwave) {
       SplitRef it;
@@ -1408,6 +1464,7 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
       g = it.g;
       k = uni(it.k);
       half = it.half;
+      pre = it.pre;
       R = it.R;
     } else {
       if (vb >= slots) return;
@@ -1427,19 +1484,21 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
       R.q0 = e1.x;
       R.s = e1.y;
       half = e1.z;
+      pre = e1.w;
       R.valid = true;
     }
-    split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds, half);
+    split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds, half, pre);
     if (P.inwave && ((vb + grid) >> P.xcd_shift) >= per_xcd) return;  // no further slot holds an item
   }
 }
 
-// Contexts of up to this many splits are merged by the short merge kernel.
+// Rows that fold up to this many splits are merged by the short merge kernel.
 constexpr int kShortMerge = 16;
 
 // ---------------------------------------------------------------------------
-// short merge (contexts of at most KS <= 16 splits): one thread per (request,
-// KV head, column, 4 consecutive d), folding the partial states in ascending
+// short merge (rows folding at most KS <= 16 splits: every split of the
+// call's contexts, or of a sliding window): one thread per (request, KV
+// head, column, 4 consecutive d), folding the partial states in ascending
 // split order with fold_scalars / fold_value; KS (4, 8 or 16) sizes the
 // registers for the call's split count.
 // ---------------------------------------------------------------------------
@@ -1457,6 +1516,7 @@ __global__ __launch_bounds__(256) void merge_short_kernel(Params P, int cols) {
   const int ncols = R.s * P.G;
   if (ncols > P.split_cols || c >= ncols) return;
   if (request_splits(R, P.window) == 1) return;  // written by the split kernel
+  if (P.casc && folds_prefix(R, P.casc_seq[r])) return;  // written by its last split's items
   // the row's splits: from the one holding its window start through its own
   const int pr = R.n - R.s + c / P.G;
   const int klo = window_lo(pr, P.window) / kSplitKeys;
@@ -1523,6 +1583,7 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
   const int ncols = R.s * P.G;
   if (ncols > P.split_cols || c >= ncols) return;
   if (request_splits(R, P.window) == 1) return;  // written by the split kernel
+  if (P.casc && folds_prefix(R, P.casc_seq[r])) return;  // written by its last split's items
   // the row's splits: from the one holding its window start through its own
   const int pr = R.n - R.s + c / P.G;
   const int klo = window_lo(pr, P.window) / kSplitKeys;
@@ -2375,14 +2436,19 @@ int run_split_phase(const Params& P, bool stream_kv, hipStream_t s, hipEvent_t e
 template <int D>
 int run_merge(const Params& P, hipStream_t s) {
   const int64_t cols = P.ws_cols;  // = min(max_q * G, split_cols)
-  if (P.max_splits <= kShortMerge) {
+  // the most splits a row folds: every split through the longest context, or
+  // with a window of w keys the splits from the one holding p - w + 1 to the
+  // one holding p, at most floor((w - 1) / 1024) + 2
+  const int fold = P.window > 0 ? std::min(P.max_splits, (P.window - 1) / kSplitKeys + 2)
+                                : P.max_splits;
+  if (fold <= kShortMerge) {
     const int64_t threads = (int64_t)P.num_seqs * P.hkv * cols * (D / 4);
     const int64_t blocks = (threads + 255) / 256;
     if (blocks > INT32_MAX) return VD_ERR_INVALID_ARG;
-    // registers for the call's split count: 4, 8 or 16 partial states
-    const auto kern = P.max_splits <= 4   ? &merge_short_kernel<D, 4>
-                      : P.max_splits <= 8 ? &merge_short_kernel<D, 8>
-                                          : &merge_short_kernel<D, 16>;
+    // registers for the rows' split count: 4, 8 or 16 partial states
+    const auto kern = fold <= 4   ? &merge_short_kernel<D, 4>
+                      : fold <= 8 ? &merge_short_kernel<D, 8>
+                                  : &merge_short_kernel<D, 16>;
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, s, P, (int)cols);
     return launched();
   }
