@@ -1093,6 +1093,9 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 // items start last.
 constexpr int kInWaveChunks = 4;
 constexpr int kInWaveMaxSeqs = 64 * kInWaveChunks;
+// At most this many requests on the chunk path are put in longest-first
+// order by the in-wave chunk planner (a pass over them per workgroup).
+constexpr int kLongestFirstReqs = 64;
 
 struct SplitRef {
   int r, g, k, half;
@@ -1239,7 +1242,13 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
 // Chunk items without a plan launch (at most kInWaveMaxSeqs requests): the
 // same one-round-trip read of the lengths, and the items of the plan's chunk
 // list -- per KV head, every q-tile of 128 query-head rows of every request
-// on the chunk path, requests ascending -- with XCD-contiguous ranges.
+// on the chunk path -- with XCD-contiguous ranges.  A workgroup's run time
+// grows with its last row's position, so when at most kLongestFirstReqs
+// requests are on the chunk path the list takes them longest first
+// (decreasing n, ties by index) and a request's q-tiles from its last: the
+// blocks of a die are dispatched in that order, which keeps the longest
+// items off the end of the launch.  Which workgroup computes a row never
+// changes its bits.
 __device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& r, int& qt,
                                                   Req& R) {
   constexpr int C = kInWaveChunks;
@@ -1275,16 +1284,48 @@ __device__ __forceinline__ bool inwave_chunk_item(const Params& P, int& g, int& 
   if (i >= total) return false;
   g = uni(i / per_head);
   const int rem = i - g * per_head;
-  int j = -1, cj = 0, off = 0, base = 0;
+  // first q-tile of each request in the list: ro
+  int ro[C];
+  int nreq = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) nreq += __builtin_popcountll(__ballot(cnt[c] > 0));
+  const bool longest_first = nreq <= kLongestFirstReqs;
+  if (longest_first) {
+#pragma unroll
+    for (int c = 0; c < C; ++c) ro[c] = 0;
+#pragma unroll
+    for (int c2 = 0; c2 < C; ++c2) {
+      uint64_t mask = __ballot(cnt[c2] > 0);
+      while (mask) {
+        const int l = __builtin_ctzll(mask);
+        mask &= mask - 1;
+        const int nl = __builtin_amdgcn_readlane(cn[c2], l);
+        const int kl = __builtin_amdgcn_readlane(cnt[c2], l);
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+          const bool before = nl > cn[c] || (nl == cn[c] && 64 * c2 + l < 64 * c + lane);
+          ro[c] += before ? kl : 0;
+        }
+      }
+    }
+  } else {
+    int base = 0;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      ro[c] = base + incl[c] - cnt[c];
+      base += __builtin_amdgcn_readlane(incl[c], 63);
+    }
+  }
+  int j = -1, cj = 0, off = 0;
 #pragma unroll
   for (int c = 0; c < C; ++c) {
-    const int tot = __builtin_amdgcn_readlane(incl[c], 63);
-    if (j < 0 && rem < base + tot) {
-      j = __builtin_ctzll(__ballot(incl[c] > rem - base));
+    const uint64_t hit = __ballot(cnt[c] > 0 && ro[c] <= rem && rem < ro[c] + cnt[c]);
+    if (j < 0 && hit) {
+      j = __builtin_ctzll(hit);
       cj = c;
-      off = rem - base - __builtin_amdgcn_readlane(incl[c] - cnt[c], j);
+      const int o = rem - __builtin_amdgcn_readlane(ro[c], j);
+      off = longest_first ? __builtin_amdgcn_readlane(cnt[c], j) - 1 - o : o;
     }
-    base += tot;
   }
   if (j < 0) return false;
   int q0 = 0, q1 = 0, n = 0;
