@@ -82,6 +82,9 @@ struct Params {
   const uint16_t* knew;
   const uint16_t* vnew;
   int fuse_write, append_wgs;
+  // a split item covers all 32 query-head rows of its split (two column
+  // blocks over one read of each tile) instead of 16
+  int wide;
   // the split workgroups derive their items from the lengths (no plan launch)
   int inwave;
   float* lse;  // optional [T, Hq] log-sum-exp output
@@ -377,12 +380,15 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 }
 
 // A split item covers 16 query-head rows ("columns") of its request: a
-// request with more (s * G in 17 .. 32) has an item per split and column half.
-__device__ __forceinline__ int column_halves(const Req& R, int G) { return R.s * G > 16 ? 2 : 1; }
+// request with more (s * G in 17 .. 32) has an item per split and column half
+// -- or, in a call with wide items, one item covering both halves.
+__device__ __forceinline__ int column_halves(const Params& P, const Req& R) {
+  return !P.wide && R.s * P.G > 16 ? 2 : 1;
+}
 
 // Length of the split work list: an upper bound of the split items.
 __host__ __device__ __forceinline__ int64_t split_slots(const Params& P) {
-  return (int64_t)P.num_seqs * P.hkv * P.max_splits * (P.split_cols / 16);
+  return (int64_t)P.num_seqs * P.hkv * P.max_splits * (P.wide ? 1 : P.split_cols / 16);
 }
 
 // Work-list entry of one split item: request, KV head, split index, the
@@ -633,7 +639,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
       if (R.valid) {
         const int ncols = R.s * P.G;
         if (ncols <= P.split_cols) {
-          h = column_halves(R, P.G);
+          h = column_halves(P, R);
           // splits before the one holding the first row's window start
           // hold no visible key and get no item
           const int lo_min = window_lo(R.n - R.s, P.window);
@@ -731,7 +737,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(Params P) {
       const int nfull = R.n / kSplitKeys;
       const int kfirst = max(window_lo(R.n - R.s, P.window) / kSplitKeys, P.casc ? csq[r] : 0);
       const int nf = nfull - kfirst;  // whole splits with items
-      const int h = column_halves(R, P.G);
+      const int h = column_halves(P, R);
       const int pre = P.casc ? csq[r] : 0;
       // items (KV head, split, half), halves adjacent
       for (int idx = lane; idx < P.hkv * nf * h; idx += 64)
@@ -1151,7 +1157,7 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
         const int nfull = R.n / kSplitKeys;
         kfst[c] = max(lo_min / kSplitKeys, ccs[c]);
         nf[c] = max(0, nfull - kfst[c]);
-        hv[c] = column_halves(R, P.G);
+        hv[c] = column_halves(P, R);
         if (R.n % kSplitKeys)
           cls[c] = (R.n + kTileKeys - 1) / kTileKeys -
                    max(nfull * kTilesPerSplit, lo_min / kTileKeys);
@@ -1236,7 +1242,7 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
   return out.r < P.num_seqs && out.g < P.hkv && out.R.valid && out.R.s * P.G <= P.split_cols &&
          out.k >= window_lo(out.R.n - out.R.s, P.window) / kSplitKeys && out.k >= cc &&
          out.k <= (out.R.n - 1) / kSplitKeys && out.half >= 0 &&
-         out.half < column_halves(out.R, P.G);
+         out.half < column_halves(P, out.R);
 }
 
 // Chunk items without a plan launch (at most kInWaveMaxSeqs requests): the
@@ -1472,13 +1478,14 @@ __device__ __forceinline__ bool append_unit(const Params& P, int u, uint16_t* ld
 }
 
 // One wavefront per workgroup, 16 columns per item (two wavefronts per SIMD
-// at head_dim 128): a finished item frees its slot at once, which keeps the
-// end of the launch short when item durations vary.  The grid is capped at
-// about twice the wavefronts the chip holds at once; workgroup b
+// at head_dim 128), or with NA = 2 (wide items) 32 columns over one read of
+// each tile (one wavefront per SIMD): a finished item frees its slot at once,
+// which keeps the end of the launch short when item durations vary.  The grid
+// is capped at about twice the wavefronts the chip holds at once; workgroup b
 // takes the slots b, b + grid, b + 2 grid, ... (the grid is a multiple of the
 // dies, so its slots stay on its XCD) until one is past the items.  NT:
 // K/V are streamed with non-temporal loads.
-template <int D, bool WIN, bool NT>
+template <int D, bool WIN, bool NT, int NA>
 __global__ __launch_bounds__(64) void split_kernel(Params P) {
   __shared__ __attribute__((aligned(16))) uint16_t vlds[kMaxNewRows * D];
   // The last append_wgs workgroups write the new tokens of the chunk-path
@@ -1528,7 +1535,7 @@ __global__ __launch_bounds__(64) void split_kernel(Params P) {
       pre = e1.w;
       R.valid = true;
     }
-    split_item<D, 1, WIN, NT>(P, r, g, k, R, vlds, half, pre);
+    split_item<D, NA, WIN, NT>(P, r, g, k, R, vlds, half, pre);
     if (P.inwave && ((vb + grid) >> P.xcd_shift) >= per_xcd) return;  // no further slot holds an item
   }
 }
@@ -2365,6 +2372,10 @@ Params make_params(const vd_attn* h, const vd_attn_batch* b, void* out, const vo
   P.max_splits = (b->max_context_len + kSplitKeys - 1) / kSplitKeys;
   P.split_cols = 16 * split_nb(h, b->max_q_len);
   P.ws_cols = ws_cols(h, b->max_q_len);
+  // wide items when every request is on the split path and some may have
+  // more than 16 rows (max_q G in 17 .. 32); a call with chunk-path rows keeps
+  // 16-row items, whose kernel holds two wavefronts per SIMD
+  P.wide = (int64_t)b->max_q_len * h->group > 16 && (int64_t)b->max_q_len * h->group <= kSplitCols;
   P.hq = h->hq;
   P.hkv = h->hkv;
   P.G = h->group;
@@ -2406,7 +2417,8 @@ int run_plan(const Params& P, hipStream_t s) {
 template <int D, bool NT>
 auto split_kernel_for(const Params& P) {
   // a handle's window is fixed at creation: one kernel per handle
-  return P.window > 0 ? &split_kernel<D, true, NT> : &split_kernel<D, false, NT>;
+  if (P.wide) return P.window > 0 ? &split_kernel<D, true, NT, 2> : &split_kernel<D, false, NT, 2>;
+  return P.window > 0 ? &split_kernel<D, true, NT, 1> : &split_kernel<D, false, NT, 1>;
 }
 
 template <int D>

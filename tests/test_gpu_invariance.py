@@ -180,14 +180,36 @@ def test_large_batch_plan_launch():
 
 def test_large_batch_column_halves():
     """More than 256 requests with 32 query-head rows per KV head (70B verify,
-    s = 4): the plan launch lists two column-half items per split.  Rows equal
-    those of a few of the requests run alone (the split workgroups' own
-    planning), and those without the shared-prefix pass."""
+    s = 4): the plan launch lists one wide item per split (both 16-row
+    blocks).  Rows equal those of a few of the requests run alone (the split
+    workgroups' own planning), and those without the shared-prefix pass."""
     big = W.config5(num_req=300, prefix=V.SPLIT_KEYS, suf_lo=20, suf_hi=300)
     a = outs(big)
     U.assert_same_bits(a, outs(big.subcall([0, 1, 150, 298, 299])), min_common=4 * 3 + 2)
     U.assert_same_bits(a, outs(big, shared_pages=False), min_common=big.total_q_tokens)
     U.say("  300 verify requests: %s" % U.parity(big, U.gpu_run(big), rows=[0, 3, 601, 749]))
+
+
+def test_wide_items_vs_column_halves():
+    """70B verify (s = 4: 32 query-head rows per KV head) runs as wide split
+    items, one per split over both 16-row blocks, when every request is on
+    the split path, and as two column-half items per split when the call also
+    carries a prefill chunk (40 G rows: the chunk path).  The verify rows are
+    the same bits either way, below and above 256 requests (in-wave planning
+    and the plan launch), with and without the shared-prefix pass; suffixes
+    up to 1500 keys give rows of up to three splits."""
+    for num_req in (12, 300):
+        base = W.config5(num_req=num_req, prefix=V.SPLIT_KEYS + 304, suf_lo=20, suf_hi=1500)
+        sh = base.shape
+        wide = outs(base)
+        extra = W.make_prompt(sh, 700, 16, 0, q_window=40)
+        mixed = W.place(sh, base.prompts + [extra], base.reqs + [W.Req(len(base.prompts), 700, 40)],
+                        W.rng_for(16, 4), shared_prefix_pages=(V.SPLIT_KEYS + 304) // sh.page_size)
+        assert mixed.max_q_len * sh.group > 32 and base.max_q_len * sh.group == 32
+        n = U.assert_same_bits(wide, outs(mixed), min_common=base.total_q_tokens)
+        n += U.assert_same_bits(wide, outs(mixed, shared_pages=False), min_common=base.total_q_tokens)
+        n += U.assert_same_bits(wide, outs(base, shared_pages=False), min_common=base.total_q_tokens)
+        U.say("  %d verify requests, wide vs column halves: %d rows bit-identical" % (num_req, n))
 
 
 def test_long_context_batch_and_placement():
