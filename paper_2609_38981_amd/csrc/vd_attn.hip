@@ -969,17 +969,19 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 #pragma unroll
   for (int b = 0; b < kPagesPerTile; ++b)
     pb[b] = page_block(P, ptrow, kt_first * kPagesPerTile + b, R.n, g);
+  // a tile holding this call's new tokens (wave-uniform)
+  auto has_new = [&](int kt) { return P.fuse_write && (kt + 1) * kTileKeys > R.n - R.s; };
+  u16x8 kf[kPagesPerTile][D / 32];
+  bool k_issued = false;  // the tile's K loads were issued during the previous tile
   for (int kt = kt_first; kt < kt_end; ++kt) {
     const int j0 = kt * kTileKeys;
     const bool full = j0 + kTileKeys <= R.n && pb[0] >= 0 && pb[1] >= 0 && pb[2] >= 0 && pb[3] >= 0;
-    u16x8 kf[kPagesPerTile][D / 32];
     u16x4 vh[D / 16][kPagesPerTile];
-    // this call's new tokens in the tile (wave-uniform)
-    const bool newtile = P.fuse_write && j0 + kTileKeys > R.n - R.s;
+    const bool newtile = has_new(kt);
     if (newtile) {
       stage_v_new<D>(P, vlds, g, R);
       load_k_new<D, NT>(P, pb, kf, j0, g, R);
-    } else {
+    } else if (!k_issued) {
       load_k<D, NT>(P, pb, kf);
     }
     // all K loads are issued before the V loads: Q.K can start on them first
@@ -994,6 +996,12 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
     if (!full) mask_k<D>(pb_cur, j0, R.n, kf);
     f32x4 acc[NA][kPagesPerTile];
     tile_scores<D, NA>([&](int b, int ks) { return kf[b][ks]; }, qf, acc);
+    // The K registers are free: the next tile's K loads fly during this
+    // tile's softmax and P.V (a tile with new tokens loads its own, after
+    // this one's; it is the request's last or next to last).
+    k_issued = kt + 1 < kt_end && !has_new(kt + 1);
+    if (k_issued) load_k<D, NT>(P, pb, kf);
+    __builtin_amdgcn_sched_barrier(0);
     if (newtile) apply_v_new<D>(P, vlds, pb_cur, vh, j0, R, half == 0);
     if (!full) mask_v<D>(pb_cur, j0, R.n, vh);
     TileWeights w[NA];
@@ -1486,7 +1494,7 @@ __device__ __forceinline__ bool append_unit(const Params& P, int u, uint16_t* ld
 // dies, so its slots stay on its XCD) until one is past the items.  NT:
 // K/V are streamed with non-temporal loads.
 template <int D, bool WIN, bool NT, int NA>
-__global__ __launch_bounds__(64) void split_kernel(Params P) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(NA == 1 || D == 64 ? 2 : 1))) void split_kernel(Params P) {
   __shared__ __attribute__((aligned(16))) uint16_t vlds[kMaxNewRows * D];
   // The last append_wgs workgroups write the new tokens of the chunk-path
   // requests (units b - grid, b - grid + append_wgs, ...): dispatched after
