@@ -1741,7 +1741,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // id mod the die count) take a contiguous range of them: the q-tiles of one
   // (request, KV head) share that XCD's L2, and with 8 KV heads on 8 dies each
   // XCD takes one head of every request, so long and short requests spread
-  // over all XCDs.
+  // over all XCDs.  (The in-wave planner lists the requests longest first.)
   int g, r, qt;
   Req R;
   if (P.inwave) {
