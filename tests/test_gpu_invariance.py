@@ -212,6 +212,37 @@ def test_wide_items_vs_column_halves():
         U.say("  %d verify requests, wide vs column halves: %d rows bit-identical" % (num_req, n))
 
 
+def test_wide_items_head_dim_64():
+    """Head dim 64, 2 query heads per KV head: 12-token verify rows (24
+    query-head rows per KV head, wide split items) against the same rows in a
+    call that also prefills a 40-token chunk (16-row column halves), and
+    against single-token steps at each position."""
+    sh = W.TINY
+    prompts = [W.make_prompt(sh, n, 17, i, q_window=12) for i, n in enumerate((700, 1500, 2100, 90))]
+    reqs = [W.Req(i, pr.length, 12) for i, pr in enumerate(prompts)]
+    wide = outs(W.place(sh, prompts, reqs, W.rng_for(17, 4)))
+    extra = W.make_prompt(sh, 300, 17, 9, q_window=40)
+    mixed = W.place(sh, prompts + [extra], reqs + [W.Req(len(prompts), 300, 40)], W.rng_for(17, 5))
+    n = U.assert_same_bits(wide, outs(mixed), min_common=48)
+    steps = [W.Req(i, pr.length - j, 1) for i, pr in enumerate(prompts) for j in range(12)]
+    n += U.assert_same_bits(wide, outs(W.place(sh, prompts, steps, W.rng_for(17, 6))), min_common=48)
+    U.say("  head dim 64, wide vs column halves vs steps: %d rows bit-identical" % n)
+
+
+def test_chunk_order_above_64_requests():
+    """70 prefill chunks (more than 64 on the chunk path: the in-wave planner
+    keeps request order) against 9 of them alone (listed longest first), and
+    in reverse order."""
+    kw = dict(chunk=96, max_off=1500, num_decode=3, dec_lo=20, dec_hi=400)
+    big = W.config3(num_prefill=70, **kw)
+    a = outs(big)
+    sub = [0, 1, 5, 17, 33, 40, 64, 69, 71]
+    n = U.assert_same_bits(a, outs(big.subcall(sub)), min_common=8 * 96 + 1)
+    rev = W.place(big.shape, big.prompts, big.reqs[::-1], W.rng_for(3, 9))
+    n += U.assert_same_bits(a, outs(rev), min_common=big.total_q_tokens)
+    U.say("  70 chunk-path requests vs 9 alone and reversed: %d rows bit-identical" % n)
+
+
 def test_long_context_batch_and_placement():
     """Config 4 family (scaled down): batch 1 vs batch 4, two placements."""
     kw = dict(lo=6000, hi=12000)
