@@ -1647,13 +1647,26 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
   const int64_t p0 = ((int64_t)(r * P.hkv + g) * P.ws_cols + c) * P.max_splits + klo;
   float carry = -__builtin_inff();  // running maximum before the chunk
   float Z = 0.f, W = 0.f;
+  // A chunk's loads are issued while the chunk before it is folded.  Every
+  // load reads one of the row's own partial states (indices past its last
+  // split are clamped to it; their values are not used), so that no load is
+  // issued under a branch.
+  float mk_n, zk_n, u_n[CH];
+  auto load_chunk = [&](int k0) {
+    mk_n = P.ws_m[p0 + min(k0 + lane, kp - 1)];
+    zk_n = P.ws_z[p0 + min(k0 + lane, kp - 1)];
+#pragma unroll
+    for (int j = 0; j < CH; ++j) u_n[j] = P.ws_u[(p0 + min(k0 + j, kp - 1)) * D + d];
+  };
+  load_chunk(0);
   for (int k0 = 0; k0 < kp; k0 += CH) {
     const bool has = k0 + lane < kp;
-    const float mk = has ? P.ws_m[p0 + k0 + lane] : -__builtin_inff();
-    const float zk = has ? P.ws_z[p0 + k0 + lane] : 0.0f;
+    const float mk = has ? mk_n : -__builtin_inff();
+    const float zk = has ? zk_n : 0.0f;
     float u[CH];
 #pragma unroll
-    for (int j = 0; j < CH; ++j) u[j] = k0 + j < kp ? P.ws_u[(p0 + k0 + j) * D + d] : 0.0f;
+    for (int j = 0; j < CH; ++j) u[j] = u_n[j];
+    load_chunk(k0 + CH);
     float pm = mk;  // inclusive prefix maximum over the chunk
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
