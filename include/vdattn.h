@@ -197,7 +197,8 @@ int vd_attn_forward_noalloc(const vd_attn* h, const vd_attn_batch* batch, void* 
  *           shared-prefix phases into the workspace (no device-to-host
  *           synchronisation);
  *   splits: rows of requests with s_r * (Hq / Hkv) <= 32 -- one work item
- *           per (request, KV head, 1024-key split, 16 query-head rows), after
+ *           per (request, KV head, 1024-key split, 16 query-head rows; 32 in
+ *           a call whose max_q_len * (Hq / Hkv) is 17..32), after
  *           the shared-prefix items (shared_pages hint) -- one per (group, KV
  *           head, 128 query-head rows of its members, shared split).  Without
  *           a plan launch, every workgroup derives its items from the lengths
