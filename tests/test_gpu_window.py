@@ -121,6 +121,26 @@ def test_window_chunking_and_query_length(shape):
     U.assert_same_bits(whole, outs(W.place(shape, [pr], reqs, rng)), min_common=600)
 
 
+@pytest.mark.parametrize("shape,w,s", [(W.TINY, 300, 12), (W.LLAMA70B, 700, 4)],
+                         ids=["tiny-w300", "70b-w700"])
+def test_window_wide_items(shape, w, s):
+    """With a window: verify rows of 17..32 query-head rows per KV head run as
+    wide split items when every request is on the split path, as column
+    halves when the call also prefills a 40-token chunk, and as single-token
+    steps: the same bits."""
+    sh = ws(shape, w)
+    assert 16 < s * sh.group <= 32
+    prompts = [W.make_prompt(sh, n, 18, i, q_window=s) for i, n in enumerate((650, 1500, 2300))]
+    reqs = [W.Req(i, pr.length, s) for i, pr in enumerate(prompts)]
+    wide = outs(W.place(sh, prompts, reqs, W.rng_for(18, 4)))
+    extra = W.make_prompt(sh, 400, 18, 9, q_window=40)
+    mixed = W.place(sh, prompts + [extra], reqs + [W.Req(len(prompts), 400, 40)], W.rng_for(18, 5))
+    n = U.assert_same_bits(wide, outs(mixed), min_common=3 * s)
+    steps = [W.Req(i, pr.length - j, 1) for i, pr in enumerate(prompts) for j in range(s)]
+    n += U.assert_same_bits(wide, outs(W.place(sh, prompts, steps, W.rng_for(18, 6))), min_common=3 * s)
+    U.say("  window %d, wide vs column halves vs steps: %d rows bit-identical" % (w, n))
+
+
 def test_window_batch_and_placement_invariance():
     """A probe request alone and at random slots of batches of 17 and 64,
     with two placements, gives the same bits under a window."""
