@@ -2013,11 +2013,13 @@ constexpr size_t prefix_lds_bytes() {
 // columns (zero queries, never stored).
 // ---------------------------------------------------------------------------
 // One item i of the list (per_head items per KV head); every value read from
-// the list is checked before it addresses memory.
-template <int D>
-__device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups, int per_head,
-                                            uint16_t* lds, int* scu) {
-  constexpr int NB = 2;
+// the list is checked before it addresses memory.  NB = 2: the item's 128
+// query-head rows (32 per wavefront); NB = 1: half of them, rows 64 half ..
+// 64 half + 63 (16 per wavefront).
+template <int D, int NB>
+__device__ __forceinline__ void prefix_item(const Params& P, int i, int half, int ngroups,
+                                            int per_head, uint16_t* lds, int* scu) {
+  static_assert(NB == 1 || NB == 2, "column blocks per wavefront");
   constexpr int BLK = kPage * D;
   constexpr int NBLK = 2 * kPagesPerTile;
   constexpr int TILE = NBLK * BLK;
@@ -2036,7 +2038,7 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
     return;
   const int t0 = P.cu[first];
   const int x = uni(rem - P.casc_off[li]);  // (tile, split) of the group
-  const int c0 = (x / cg) * kChunkCols, k = x % cg;
+  const int c0 = (x / cg) * kChunkCols + half * 64 * NB, k = x % cg;
   const int ncols = (P.cu[end] - t0) * P.G;
   if (c0 < 0 || c0 >= ncols) return;
   // the requests of the item's rows: consecutive, from the one holding its
@@ -2059,7 +2061,7 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
   State<D> st[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int c = c0 + wave * 32 + nb * 16 + col;
+    const int c = c0 + wave * 16 * NB + nb * 16 + col;
     bool v = c < ncols;
     int t = 0, hh = 0;
     pidx[nb] = 0;
@@ -2081,7 +2083,10 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
     load_q<D>(P, qf[nb], v ? t : 0, g * P.G + (v ? hh : 0), v);
     state_init(st[nb]);
   }
-  const bool wave_live = __any(live[0] || live[1]);
+  bool any_live = false;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) any_live = any_live || live[nb];
+  const bool wave_live = __any(any_live);
 
   // the page ids of tile kt (-1: no page), one broadcast LDS read
   auto tile_pages = [&](int kt) {
@@ -2179,7 +2184,10 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int ngroups,
 
 // Items: KV head major, then listed group, then (tile, split).  Each XCD
 // (workgroup id mod the die count) takes a contiguous share of the list, which its
-// workgroups run in turn: the grid is sized to the chip, not to the list.
+// workgroups run in turn: the grid is sized to the chip, not to the list.  When
+// the share's last round would fill at most half of the die's workgroups, each
+// of its items runs as two halves of 64 query-head rows on two workgroups: the
+// same per-column operations, on twice as many compute units.
 template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefix_kernel(Params P) {
   // [STAGES][8 page blocks], then the page ids of an item's split
@@ -2189,10 +2197,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   if (ngroups < 1 || ngroups > P.num_seqs / 2 || per_head < 1 || per_head > (1 << 24)) return;
   const int total = per_head * P.hkv;
   const int per_xcd = (total + P.xcds - 1) >> P.xcd_shift;
-  for (int j = (int)(blockIdx.x >> P.xcd_shift); j < per_xcd; j += (int)(gridDim.x >> P.xcd_shift)) {
+  const int slots = (int)(gridDim.x >> P.xcd_shift);  // workgroups of a die
+  const int base = (per_xcd - 1) / slots * slots;       // items before the last round
+  const int last = per_xcd - base;
+  const bool halve = 2 * last <= slots;
+  const int entries = halve ? base + 2 * last : per_xcd;
+  for (int e = (int)(blockIdx.x >> P.xcd_shift); e < entries; e += slots) {
+    const bool part = halve && e >= base;
+    const int j = part ? base + (e - base) / 2 : e;
     const int i = uni((int)(blockIdx.x & (P.xcds - 1)) * per_xcd + j);
     if (i >= total) break;
-    prefix_item<D>(P, i, ngroups, per_head, lds, scu);
+    if (part)
+      prefix_item<D, 1>(P, i, (e - base) % 2, ngroups, per_head, lds, scu);
+    else
+      prefix_item<D, 2>(P, i, 0, ngroups, per_head, lds, scu);
     __syncthreads();  // LDS (ring, scu) is free for the next item
   }
 }
