@@ -1209,8 +1209,16 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
     }
   } else {
     idx -= whole;
+    // the tile counts some request's last split has (bit t), longest first
+    int bits = 0;
 #pragma unroll
-    for (int t = kTilesPerSplit; t >= 1; --t)
+    for (int c = 0; c < C; ++c) bits |= cls[c] > 0 ? 1 << cls[c] : 0;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) bits |= __shfl_xor(bits, o, 64);
+    unsigned present = uni(bits);
+    while (present && j < 0) {
+      const int t = 31 - __builtin_clz(present);
+      present &= ~(1u << t);
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         const unsigned long long m = __ballot(cls[c] == t);
@@ -1228,6 +1236,7 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
           }
         }
       }
+    }
   }
   if (j < 0) return false;
   int q0 = 0, q1 = 0, n = 0, cc = 0;
@@ -2470,9 +2479,10 @@ int run_splits(const Params& P0, bool stream_kv, hipStream_t s, hipEvent_t e0 = 
   const int64_t items = split_slots(P);
   if (items > INT32_MAX - 8) return VD_ERR_INVALID_ARG;
   // at most about twice the wavefronts the chip holds at once (4 SIMDs per
-  // compute unit, two wavefronts each); a multiple of the dies
+  // compute unit, two wavefronts each -- one for wide items at head dim
+  // 128); a multiple of the dies
   const Geometry geo = device_geometry();
-  const int64_t cap = 16 * (int64_t)geo.cus;
+  const int64_t cap = (P.wide && D == 128 ? 8 : 16) * (int64_t)geo.cus;
   const int64_t split_wgs = (std::min(items, cap) + geo.xcds - 1) / geo.xcds * geo.xcds;
   // the chunk-path requests' new tokens: a workgroup per unit up to the cap
   // (an upper bound of the units: every request's page runs number at most
