@@ -1706,6 +1706,37 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
   if (P.lse && d == 0) P.lse[row] = final_lse(carry, Z);  // carry: the maximum over every split
 }
 
+// Issue order of a tile's LDS reads against its matrix instructions in the
+// chunk and shared-prefix kernels (scheduling hints only: every accumulator's
+// chain of instructions, and so every bit, is the same).  Without them the
+// compiler keeps two K reads ahead of Q.K and one d-block's V reads ahead of
+// P.V, and waits on each.  Q.K: four of the tile's kPagesPerTile * D / 32 K
+// reads first, then one read per NB matrix instructions.  P.V: the V reads of
+// two d-blocks first, then one d-block's (four reads) per d-block of matrix
+// instructions (2 NB).
+template <int D, int NB>
+__device__ __forceinline__ void order_qk_reads() {
+  constexpr int R = kPagesPerTile * (D / 32), A = 4;
+  __builtin_amdgcn_sched_group_barrier(0x100, A, 0);  // DS reads
+#pragma unroll
+  for (int i = A; i < R; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, NB, 0);  // matrix instructions
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, NB * A, 0);
+}
+template <int D, int NB>
+__device__ __forceinline__ void order_pv_reads() {
+  constexpr int MB = D / 16;  // d-blocks, four V reads and 2 NB matrix instructions each
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+  for (int m = 2; m < MB; ++m) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);
+}
+
 // ---------------------------------------------------------------------------
 // chunk kernel: one workgroup (4 wavefronts x 32 columns) per
 // (request, KV head, 128 query-head rows).  The request's K/V tiles stream
@@ -1935,6 +1966,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       tile_scores<D, NB>(
           [&](int b, int ks) { return *reinterpret_cast<const u16x8*>(T + b * BLK + 512 * ks + 8 * lane); },
           qf, acc);
+      order_qk_reads<D, NB>();
       __builtin_amdgcn_s_setprio(0);
       TileWeights w[NB];
       bool open = true;  // every key of the tile visible to every column
@@ -1959,6 +1991,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) tile_pv_block<D>(st[nb], w[nb], m, v0, v1);
       }
+      order_pv_reads<D, NB>();
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) tile_commit<D>(st[nb], w[nb]);
       __builtin_amdgcn_s_setprio(0);
@@ -2161,10 +2194,13 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int half, in
       tile_scores<D, NB>(
           [&](int b, int ks) { return *reinterpret_cast<const u16x8*>(T + b * BLK + 512 * ks + 8 * lane); },
           qf, acc);
+      order_qk_reads<D, NB>();
+      __builtin_amdgcn_sched_barrier(0);  // Q.K, the softmax and P.V are scheduled apart
       // every key of a shared split is visible to every member column
       TileWeights w[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) w[nb] = tile_softmax<D, false, false>(st[nb], acc[nb], j0, 0, 0, P.c);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int m = 0; m < D / 16; ++m) {
         const int o = 256 * m + 4 * lane;
@@ -2173,6 +2209,7 @@ __device__ __forceinline__ void prefix_item(const Params& P, int i, int half, in
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) tile_pv_block<D>(st[nb], w[nb], m, v0, v1);
       }
+      order_pv_reads<D, NB>();
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) tile_commit<D>(st[nb], w[nb]);
     }

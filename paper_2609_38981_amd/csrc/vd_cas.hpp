@@ -74,11 +74,37 @@ __device__ __forceinline__ uint16_t bf16_out(float f) {
 
 __device__ __forceinline__ float fmax_(float a, float b) { return __builtin_fmaxf(a, b); }
 
-// Cross-lane exchange with lane l ^ mask (mask 16 or 32), via ds_bpermute.
-__device__ __forceinline__ float xor_lane(float v, int mask) {
-  const int lane = __lane_id();
-  return __builtin_bit_cast(
-      float, __builtin_amdgcn_ds_bpermute((lane ^ mask) << 2, __builtin_bit_cast(int, v)));
+// Row exchanges of the vector ALU (a row is 16 lanes): v_permlane16_swap
+// trades the odd rows of its first register with the even rows of its second,
+// v_permlane32_swap the upper half of the first with the lower half of the
+// second.  Both registers holding x, the first then holds the even row (lower
+// half) of every pair of lanes l, l ^ 16 (l, l ^ 32) and the second the odd
+// row (upper half).  The two wait states before each swap are its hazard
+// after a vector-ALU write of either register.  Every lane of the wavefront
+// must be active (the callers' tile loops are wave-uniform).
+__device__ __forceinline__ void swap_rows16(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void swap_rows32(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+
+// The maximum (sum) over the four lanes of a column, l, l ^ 16, l ^ 32 and
+// l ^ 48, in every one of them: first each pair of rows (even, odd), then the
+// two halves (lower, upper) -- the operands always in that order.
+__device__ __forceinline__ float column_max(float x) {
+  float a = x, b = x;
+  swap_rows16(a, b);
+  a = b = fmax_(a, b);
+  swap_rows32(a, b);
+  return fmax_(a, b);
+}
+__device__ __forceinline__ float column_sum(float x) {
+  float a = x, b = x;
+  swap_rows16(a, b);
+  a = b = a + b;
+  swap_rows32(a, b);
+  return a + b;
 }
 
 // Online-softmax state of one column (replicated in the 4 lanes of the
@@ -170,8 +196,7 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
     t[b] = fmax_(fmax_(g0, g1), fmax_(g2, g3));
   }
   float mx = fmax_(fmax_(t[0], t[1]), fmax_(t[2], t[3]));
-  mx = fmax_(mx, xor_lane(mx, 16));
-  mx = fmax_(mx, xor_lane(mx, 32));
+  mx = column_max(mx);
   TileWeights w;
   w.h = !MASKED || (j0 <= p && (!WIN || j0 + kTileKeys - 1 >= lo));  // any visible key
   w.m_new = fmax_(st.m, mx);
@@ -193,8 +218,7 @@ __device__ __forceinline__ TileWeights tile_softmax(const State<D>& st,
 #pragma unroll
   for (int b = 0; b < kPagesPerTile; ++b) sb[b] = (a[b][0] + a[b][1]) + (a[b][2] + a[b][3]);
   float s = (sb[0] + sb[1]) + (sb[2] + sb[3]);
-  s = s + xor_lane(s, 16);
-  s = s + xor_lane(s, 32);
+  s = column_sum(s);
   w.z_new = st.z * w.alpha + s;
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh)

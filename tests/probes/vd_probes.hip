@@ -7,7 +7,12 @@
 //                  A [tiles][16][32] bf16, B [tiles][32][16] bf16,
 //                  C, D [tiles][16][16] fp32 (row-major, device memory).
 //   vdp_exp2:      y[i] = v_exp_f32(x[i]).
-//   vdp_cvt_bf16:  y[i] = v_cvt_pk_bf16_f32(x[i]) (bf16 bits), n even.
+//   vdp_cvt_bf16:  y[i] = v_cvt_pk_bf16_f32(x[i]) (bf16 bits).
+//   vdp_row_swap:  one wavefront: v_permlane16_swap_b32 and
+//                  v_permlane32_swap_b32 on the registers (a[l], b[l]),
+//                  written as out[0..63] / out[64..127] (first and second
+//                  register after the 16-lane swap) and out[128..191] /
+//                  out[192..255] (after the 32-lane swap); a, b [64] fp32.
 //
 // Every entry point returns 0, or -1 for a bad size or pointer (nothing is
 // launched then), or -2 if the launch failed.  One wavefront per tile or per
@@ -56,6 +61,19 @@ __global__ __launch_bounds__(64) void cvt_bf16_kernel(const float* x, uint16_t* 
   if (i < n) y[i] = __builtin_bit_cast(uint16_t, (__bf16)x[i]);
 }
 
+// The attention kernels' row exchanges, with the same two wait states before
+// each swap.
+__global__ __launch_bounds__(64) void row_swap_kernel(const float* a, const float* b, float* out) {
+  const int l = threadIdx.x;
+  float a16 = a[l], b16 = b[l], a32 = a[l], b32 = b[l];
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a16), "+v"(b16));
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a32), "+v"(b32));
+  out[l] = a16;
+  out[64 + l] = b16;
+  out[128 + l] = a32;
+  out[192 + l] = b32;
+}
+
 int launched() { return hipGetLastError() == hipSuccess ? 0 : -2; }
 
 }  // namespace
@@ -85,6 +103,13 @@ int vdp_cvt_bf16(const void* x, void* y, int64_t n, hipStream_t stream) {
   if (n == 0) return 0;
   hipLaunchKernelGGL(cvt_bf16_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, stream,
                      static_cast<const float*>(x), static_cast<uint16_t*>(y), n);
+  return launched();
+}
+
+int vdp_row_swap(const void* a, const void* b, void* out, hipStream_t stream) {
+  if (!a || !b || !out) return -1;
+  hipLaunchKernelGGL(row_swap_kernel, dim3(1), dim3(64), 0, stream, static_cast<const float*>(a),
+                     static_cast<const float*>(b), static_cast<float*>(out));
   return launched();
 }
 

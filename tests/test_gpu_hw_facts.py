@@ -15,6 +15,10 @@ built by __graft_entry__.build()) and checking their results on the host.
 * v_exp_f32: exp2(+-0) = 1, exp2(-inf) = 0 (the identity and masked steps of
   the softmax), and results below the normal range are flushed to +0.
 * v_cvt_pk_bf16_f32: round to nearest, ties to even (the P operand's cast).
+* v_permlane16_swap_b32 / v_permlane32_swap_b32 (the softmax's exchanges
+  between the four lanes of a column): the odd 16-lane rows of the first
+  register trade places with the even rows of the second, and the upper half
+  of the first with the lower half of the second.
 """
 from __future__ import annotations
 
@@ -42,7 +46,8 @@ def probes():
     lib.vdp_mfma_bf16.argtypes = [vp, vp, vp, vp, ctypes.c_int, vp]
     lib.vdp_exp2.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.vdp_cvt_bf16.argtypes = [vp, vp, ctypes.c_int64, vp]
-    for f in (lib.vdp_mfma_bf16, lib.vdp_exp2, lib.vdp_cvt_bf16):
+    lib.vdp_row_swap.argtypes = [vp, vp, vp, vp]
+    for f in (lib.vdp_mfma_bf16, lib.vdp_exp2, lib.vdp_cvt_bf16, lib.vdp_row_swap):
         f.restype = ctypes.c_int
     return lib
 
@@ -245,3 +250,24 @@ def test_cvt_bf16_rounds_to_nearest_even(probes):
     bad = int(np.sum(got != rne_bf16_reference(x)))
     U.say("  cvt to bf16: %d of %d differ from nearest-even (%d exact ties)" % (bad, n, n // 2))
     assert bad == 0
+
+
+def test_row_swaps_exchange_rows_between_two_registers(probes):
+    a = np.arange(64, dtype=np.float32)
+    b = 1000.0 + np.arange(64, dtype=np.float32)
+    da, db = torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()
+    out = torch.zeros(256, dtype=torch.float32, device="cuda")
+    assert probes.vdp_row_swap(da.data_ptr(), db.data_ptr(), out.data_ptr(), _stream()) == 0
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().reshape(4, 64)
+    r = lambda x, k: x[16 * k: 16 * k + 16]  # noqa: E731  (row k of 16 lanes)
+    # 16-lane swap: odd rows of the first register <-> even rows of the second
+    want_a16 = np.concatenate([r(a, 0), r(b, 0), r(a, 2), r(b, 2)])
+    want_b16 = np.concatenate([r(a, 1), r(b, 1), r(a, 3), r(b, 3)])
+    # 32-lane swap: upper half of the first <-> lower half of the second
+    want_a32 = np.concatenate([a[:32], b[:32]])
+    want_b32 = np.concatenate([a[32:], b[32:]])
+    for name, g, w in (("first after 16", got[0], want_a16), ("second after 16", got[1], want_b16),
+                       ("first after 32", got[2], want_a32), ("second after 32", got[3], want_b32)):
+        U.say("  row swap, %s register: %s" % (name, "as expected" if np.array_equal(g, w) else g))
+        assert np.array_equal(g, w)
