@@ -1,14 +1,15 @@
 """GPU: seeded random batches across the shapes and call options the library
-takes -- head dim 64 and 128, 1 to 8 query heads per KV head, sliding windows,
-a shared prefix with and without the shared_pages hint, new tokens handed
-over in k_new / v_new, batch sizes on both sides of the in-wave planners'
-limits (64 and 256 requests) -- with query lengths mixing decode (s = 1),
-verify (s up to 16) and prefill chunks (up to 600).  In every case the rows
-of a few requests run alone are bit-identical to their rows in the batch
-(the causal contract of the paper's Section 5.3 / Appendix A.1), and sampled
-rows match the oracle within the parity tolerance.  New tokens are kept off
-the shared prefix pages: a call may not read one request's new-token slot
-as another request's key (Section 4.1: new tokens go to private slots)."""
+takes -- head dim 64 and 128, 1 to 12 query heads per KV head (3, 7 and 12
+among them: groups need not be powers of two), sliding windows, a shared
+prefix with and without the shared_pages hint, new tokens handed over in
+k_new / v_new, batch sizes on both sides of the in-wave planners' limits (64
+and 256 requests) -- with query lengths mixing decode (s = 1), verify (s up
+to 16) and prefill chunks (up to 600).  In every case the rows of a few
+requests run alone are bit-identical to their rows in the batch (the causal
+contract of the paper's Section 5.3 / Appendix A.1), and sampled rows match
+the oracle within the parity tolerance.  New tokens are kept off the shared
+prefix pages: a call may not read one request's new-token slot as another
+request's key (Section 4.1: new tokens go to private slots)."""
 from __future__ import annotations
 
 import numpy as np
@@ -30,6 +31,11 @@ CASES = [
     ("d128-g4-3req-long", W.Shape(32, 8, 128), 3, False, None, False),
     ("d128-g8-255req-prefix-append", W.Shape(64, 8, 128), 255, True, False, True),
     ("d64-g2-256req-prefix-hint-append", W.Shape(4, 2, 64), 256, True, True, True),
+    # groups that are not powers of two
+    ("d64-g3-63req", W.Shape(6, 2, 64), 63, False, None, False),
+    ("d128-g7-100req-append", W.Shape(28, 4, 128), 100, False, None, True),
+    ("d128-g12-64req-prefix-hint", W.Shape(24, 2, 128), 64, True, True, False),
+    ("d64-g7-257req-window-append", W.Shape(21, 3, 64, window=2500), 257, False, None, True),
 ]
 
 
