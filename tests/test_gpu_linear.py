@@ -123,3 +123,27 @@ def test_linear_full_size_sampled():
     U.say("linear full size: %s" % (_check_parity(a, b, full, rows=rows),))
     for x in rows[1:]:
         assert np.array_equal(_gpu_linear(a[x:x + 1], b)[0], full[x]), x
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_linear_random_shapes(case):
+    """Seeded random shapes (N off every tile multiple among them, K up to
+    4096, padded row strides): sampled rows within the bound of the oracle,
+    rows bit-identical computed in another M at other positions, columns
+    bit-identical computed from a subset of the weight rows."""
+    rng = np.random.default_rng(8100 + case)
+    M = int(rng.choice([1, 17, 65, 255, 257, 1000]))
+    N = int(rng.choice([8, 17, 95, 97, 193, 1000, 4095]))
+    K = 64 * int(rng.integers(1, 65))
+    lda = K + 8 * int(rng.choice([0, 1, 5]))
+    a, b = _draw(8200 + case, M, N, K)
+    got = _gpu_linear(a, b, lda=lda)
+    rows = rng.choice(M, size=min(4, M), replace=False)
+    err, rel = _check_parity(a, b, got, rows=rows)
+    sub = np.sort(rng.choice(M, size=min(M, 20), replace=False))
+    perm = rng.permutation(len(sub))
+    assert np.array_equal(_gpu_linear(np.ascontiguousarray(a[sub][perm]), b), got[sub][perm])
+    cols = np.sort(rng.choice(N, size=min(N, 24), replace=False))
+    assert np.array_equal(_gpu_linear(a, np.ascontiguousarray(b[cols])), got[:, cols])
+    U.say("linear %dx%dx%d (lda %d): max abs err %.3g; %d rows and %d columns bit-identical" % (
+        M, N, K, lda, err, len(sub), len(cols)))
