@@ -150,8 +150,8 @@ typedef struct {
 } vd_attn_batch;
 
 /* Bytes of workspace one call needs for the given host-side sizes: the plan
- * (int32 arrays of about 3 num_seqs, the shared-prefix list and the split work
- * list) and, for every (request, KV head, query-head row < min(max_q_len *
+ * (int32 arrays of about 3 num_seqs, the shared-prefix list, the split work
+ * list and the split launch's slot counter) and, for every (request, KV head, query-head row < min(max_q_len *
  * Hq / Hkv, 32), 1024-key split < ceil(max_context_len / 1024)), a partial
  * state of head_dim + 2 floats. */
 int vd_attn_workspace_size(const vd_attn* h, int32_t num_seqs, int32_t max_q_len,
@@ -204,9 +204,13 @@ int vd_attn_forward_noalloc(const vd_attn* h, const vd_attn_batch* batch, void* 
  *           a plan launch, every workgroup derives its items from the lengths
  *           and the call's new tokens are written by this launch: the items
  *           write their own requests' rows, and further workgroups, after
- *           the items', those of the requests of the chunks phase.  A request
- *           with one split writes its output rows directly; otherwise each
- *           item writes a partial state;
+ *           the items', those of the requests of the chunks phase.  When the
+ *           call can have more items than the launch has workgroups (and its
+ *           K/V stream past the caches: no shared_pages hint), a one-wavefront
+ *           launch first zeroes a counter in the workspace, from which the
+ *           workgroups claim the items past their first.  A request with one
+ *           split writes its output rows directly; otherwise each item writes
+ *           a partial state;
  *   chunks: rows of requests with s_r * (Hq / Hkv) > 32 -- one work item per
  *           (request, KV head, 128 query-head rows); folds the splits in
  *           registers and writes their output rows;

@@ -96,6 +96,10 @@ struct Params {
   int32_t* casc_seq;  // [num_seqs] leading splits of the request computed by it (0: none)
   int32_t* casc_off;  // [listed groups + 1] first item of each group
   int4* casc_grp;     // [listed groups] {first member, last member + 1, splits, first token}
+  // split slots past the first grid are claimed from this counter, zeroed by
+  // a fill launch just before the split launch (nullptr: every workgroup runs
+  // the slots b, b + grid, ... of its own die)
+  int32_t* claim;
 };
 
 struct Req {
@@ -1517,14 +1521,32 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(NA == 1 || D
     return;
   }
   const int64_t slots = split_slots(P);  // work-list length
+  // Slots b, then (claimed, when the call has more items than workgroups)
+  // grid + 0, grid + 1, ...: a workgroup whose die the memory serves faster
+  // runs more of the later items.  Claims grow, so the first claimed slot
+  // past the last die range ends a workgroup's run.
+  bool claims = P.inwave && P.claim != nullptr;
+  auto claim = [&]() {
+    int c = 0;
+    if (__lane_id() == 0) c = atomicAdd(P.claim, 1);
+    return grid + uni(c);
+  };
   int per_xcd = 0;
-  for (int vb = blockIdx.x;; vb += grid) {
+  for (int vb = blockIdx.x;;) {
     int r, g, k, half, pre;
     Req R;
     if (P.inwave) {
       SplitRef it;
-      if (!inwave_split_item(P, vb, it)) return;
+      const bool found = inwave_split_item(P, vb, it);
       per_xcd = it.per_xcd;
+      claims = claims && (per_xcd << P.xcd_shift) > grid;
+      if (!found) {
+        // a slot with no item: past the last die range, or (claimed slots)
+        // one of the last die's unused slots, after which others follow
+        if (!claims || (vb >> P.xcd_shift) >= per_xcd) return;
+        vb = claim();
+        continue;
+      }
       r = uni(it.r);
       g = it.g;
       k = uni(it.k);
@@ -1537,7 +1559,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(NA == 1 || D
       // the exit test and the item's fields cost a single round trip (the
       // list is read-only for the whole launch)
       typedef int int8v __attribute__((ext_vector_type(8)));
-      const int32_t* ep = P.items + (int64_t)vb * kItemInts;
+      const int32_t* ep = P.items + (int64_t)uni(vb) * kItemInts;
       int8v ev;
       asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(ev) : "s"(ep) : "memory");
       const int4 e0 = int4{ev[0], ev[1], ev[2], ev[3]}, e1 = int4{ev[4], ev[5], ev[6], ev[7]};
@@ -1553,8 +1575,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(NA == 1 || D
       R.valid = true;
     }
     split_item<D, NA, WIN, NT>(P, r, g, k, R, vlds, half, pre);
-    if (P.inwave && ((vb + grid) >> P.xcd_shift) >= per_xcd) return;  // no further slot holds an item
+    if (claims) {
+      vb = claim();
+      if ((vb >> P.xcd_shift) >= per_xcd) return;
+    } else {
+      if (P.inwave && ((vb + grid) >> P.xcd_shift) >= per_xcd) return;  // no further slot holds an item
+      vb += grid;
+    }
   }
+}
+
+// Zeroes the split launch's slot counter (a kernel rather than a memset, so
+// that a captured graph replays it like the launches around it).
+__global__ __launch_bounds__(64) void zero_claim_kernel(int32_t* claim) {
+  if (threadIdx.x == 0) *claim = 0;
 }
 
 // Rows that fold up to this many splits are merged by the short merge kernel.
@@ -1676,28 +1710,41 @@ __global__ __launch_bounds__(64) void merge_long_kernel(Params P, int cols) {
 #pragma unroll
     for (int j = 0; j < CH; ++j) u[j] = u_n[j];
     load_chunk(k0 + CH);
-    float pm = mk;  // inclusive prefix maximum over the chunk
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const float t = __shfl_up(pm, o, 64);
-      if (lane >= o) pm = fmax_(pm, t);
-    }
+    // inclusive prefix maximum over the chunk: DPP row shifts, then row broadcasts
+    const int ninf = __builtin_bit_cast(int, -__builtin_inff());
+    int xb = __builtin_bit_cast(int, mk);
+    auto mstep = [&](int t) { xb = __builtin_bit_cast(int, fmax_(__builtin_bit_cast(float, xb), __builtin_bit_cast(float, t))); };
+    mstep(__builtin_amdgcn_update_dpp(ninf, xb, 0x111, 0xf, 0xf, false));
+    mstep(__builtin_amdgcn_update_dpp(ninf, xb, 0x112, 0xf, 0xf, false));
+    mstep(__builtin_amdgcn_update_dpp(ninf, xb, 0x114, 0xf, 0xf, false));
+    mstep(__builtin_amdgcn_update_dpp(ninf, xb, 0x118, 0xf, 0xf, false));
+    mstep(__builtin_amdgcn_update_dpp(ninf, xb, 0x142, 0xa, 0xf, false));
+    mstep(__builtin_amdgcn_update_dpp(ninf, xb, 0x143, 0xc, 0xf, false));
+    const float pm = __builtin_bit_cast(float, xb);
     const float Mk = fmax_(carry, pm);  // M after split k0 + lane
-    float Mp = __shfl_up(Mk, 1, 64);    // M before it
-    if (lane == 0) Mp = carry;
+    // M before it: lane l - 1's (wave shift right), the carry in lane 0
+    const float Mp = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+        __builtin_bit_cast(int, carry), __builtin_bit_cast(int, Mk), 0x138, 0xf, 0xf, false));
     const float a = ex2(Mp - Mk), b = ex2(mk - Mk);
-#pragma unroll
-    for (int j = 0; j < CH; ++j) {
-      if (k0 + j < kp) {
-        if (k0 + j == 0) {
-          W = u[0];
-          Z = readlane_f(zk, 0);
-        } else {
-          const float aj = readlane_f(a, j), bj = readlane_f(b, j);
-          Z = Z * aj + readlane_f(zk, j) * bj;
-          W = fold_value(W, u[j], FoldScalars{0.f, 0.f, aj, bj});
-        }
+    // one fold step: split k0 + j (the first split of the row starts the state)
+    auto step = [&](int j) {
+      if (k0 + j == 0) {
+        W = u[0];
+        Z = readlane_f(zk, 0);
+      } else {
+        const float aj = readlane_f(a, j), bj = readlane_f(b, j);
+        Z = Z * aj + readlane_f(zk, j) * bj;
+        W = fold_value(W, u[j], FoldScalars{0.f, 0.f, aj, bj});
       }
+    };
+    if (k0 + CH <= kp) {
+      // a whole chunk: no test between the steps
+#pragma unroll
+      for (int j = 0; j < CH; ++j) step(j);
+    } else {
+#pragma unroll
+      for (int j = 0; j < CH; ++j)
+        if (k0 + j < kp) step(j);
     }
     carry = readlane_f(Mk, CH - 1);
   }
@@ -2321,6 +2368,10 @@ namespace {
 size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 
+// The split launch's slot counter: an int32 of the workspace header's 256
+// bytes, after the shared-prefix plan's two.
+constexpr int kClaimWord = 16;
+
 struct WsLayout {
   size_t off_full, off_part, off_chunk, casc_hdr, casc_seq, casc_off, casc_grp, items, m_off,
       z_off, u_off, total;
@@ -2530,6 +2581,23 @@ int run_splits(const Params& P0, bool stream_kv, hipStream_t s, hipEvent_t e0 = 
     append = (std::min(units, cap) + geo.xcds - 1) / geo.xcds * geo.xcds;
   }
   P.append_wgs = (int)append;
+  // Calls that can have more items than workgroups take the later ones from
+  // a counter in the workspace header, when the items derive their own slots
+  // and the K/V stream past the caches (with shared pages, each die keeps its
+  // own KV head's range, whose pages stay in its L2).  The items of a request
+  // and KV head: its splits from the one holding its first row's window
+  // start (at most (window + s - 2) / 1024 + 2 of them), times its column
+  // halves.
+  const int64_t req_splits =
+      P.window > 0 ? std::min<int64_t>(P.max_splits, ((int64_t)P.window + P.max_q - 2) / kSplitKeys + 2)
+                   : P.max_splits;
+  const int64_t item_bound = (int64_t)P.num_seqs * P.hkv * req_splits *
+                             (!P.wide && (int64_t)P.max_q * P.G > 16 ? 2 : 1);
+  P.claim = nullptr;
+  if (P.inwave && stream_kv && !P.casc && item_bound > split_wgs) {
+    P.claim = P.casc_hdr + kClaimWord;
+    hipLaunchKernelGGL(zero_claim_kernel, dim3(1), dim3(64), 0, s, P.claim);
+  }
   const dim3 grid((unsigned)(split_wgs + append)), block(64);
   const auto kern = stream_kv ? split_kernel_for<D, true>(P) : split_kernel_for<D, false>(P);
   hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, P);

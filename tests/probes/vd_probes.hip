@@ -13,6 +13,11 @@
 //                  written as out[0..63] / out[64..127] (first and second
 //                  register after the 16-lane swap) and out[128..191] /
 //                  out[192..255] (after the 32-lane swap); a, b [64] fp32.
+//   vdp_claims:    wgs one-wavefront workgroups (spread over every die), each
+//                  taking per values from one counter with atomicAdd(c, 1)
+//                  from lane 0 (the split launch's slot claims); out [wgs *
+//                  per] int32 gets them in claim order, counter [1] int32 is
+//                  zeroed by a fill launch first.
 //
 // Every entry point returns 0, or -1 for a bad size or pointer (nothing is
 // launched then), or -2 if the launch failed.  One wavefront per tile or per
@@ -74,6 +79,19 @@ __global__ __launch_bounds__(64) void row_swap_kernel(const float* a, const floa
   out[192 + l] = b32;
 }
 
+__global__ __launch_bounds__(64) void zero_kernel(int32_t* c) {
+  if (threadIdx.x == 0) *c = 0;
+}
+
+__global__ __launch_bounds__(64) void claims_kernel(int32_t* c, int32_t* out, int per) {
+  for (int i = 0; i < per; ++i) {
+    int v = 0;
+    if (threadIdx.x == 0) v = atomicAdd(c, 1);
+    v = __builtin_amdgcn_readfirstlane(v);
+    if (threadIdx.x == 0) out[(int64_t)blockIdx.x * per + i] = v;
+  }
+}
+
 int launched() { return hipGetLastError() == hipSuccess ? 0 : -2; }
 
 }  // namespace
@@ -110,6 +128,14 @@ int vdp_row_swap(const void* a, const void* b, void* out, hipStream_t stream) {
   if (!a || !b || !out) return -1;
   hipLaunchKernelGGL(row_swap_kernel, dim3(1), dim3(64), 0, stream, static_cast<const float*>(a),
                      static_cast<const float*>(b), static_cast<float*>(out));
+  return launched();
+}
+
+int vdp_claims(void* counter, void* out, int wgs, int per, hipStream_t stream) {
+  if (!counter || !out || wgs < 1 || wgs > (1 << 20) || per < 1 || per > 64) return -1;
+  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(64), 0, stream, static_cast<int32_t*>(counter));
+  hipLaunchKernelGGL(claims_kernel, dim3((unsigned)wgs), dim3(64), 0, stream,
+                     static_cast<int32_t*>(counter), static_cast<int32_t*>(out), per);
   return launched();
 }
 

@@ -19,6 +19,9 @@ built by __graft_entry__.build()) and checking their results on the host.
   between the four lanes of a column): the odd 16-lane rows of the first
   register trade places with the even rows of the second, and the upper half
   of the first with the lower half of the second.
+* atomicAdd on a device-memory int32 (a vector atomic at agent scope): the
+  values workgroups on all eight dies take from one counter are each handed
+  out once, 0 .. N - 1 -- the split launch claims its later slots this way.
 """
 from __future__ import annotations
 
@@ -47,7 +50,8 @@ def probes():
     lib.vdp_exp2.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.vdp_cvt_bf16.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.vdp_row_swap.argtypes = [vp, vp, vp, vp]
-    for f in (lib.vdp_mfma_bf16, lib.vdp_exp2, lib.vdp_cvt_bf16, lib.vdp_row_swap):
+    lib.vdp_claims.argtypes = [vp, vp, ctypes.c_int, ctypes.c_int, vp]
+    for f in (lib.vdp_mfma_bf16, lib.vdp_exp2, lib.vdp_cvt_bf16, lib.vdp_row_swap, lib.vdp_claims):
         f.restype = ctypes.c_int
     return lib
 
@@ -271,3 +275,20 @@ def test_row_swaps_exchange_rows_between_two_registers(probes):
                        ("first after 32", got[2], want_a32), ("second after 32", got[3], want_b32)):
         U.say("  row swap, %s register: %s" % (name, "as expected" if np.array_equal(g, w) else g))
         assert np.array_equal(g, w)
+
+
+@pytest.mark.parametrize("wgs,per", [(4096, 4), (20000, 1)])
+def test_counter_claims_are_unique_across_dies(probes, wgs, per):
+    counter = torch.full((1,), -7, dtype=torch.int32, device="cuda")
+    out = torch.full((wgs * per,), -1, dtype=torch.int32, device="cuda")
+    for rep in range(3):
+        assert probes.vdp_claims(counter.data_ptr(), out.data_ptr(), wgs, per, _stream()) == 0
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        ok = np.array_equal(np.sort(got), np.arange(wgs * per))
+        U.say("  %d workgroups x %d claims, run %d: %s; counter ends at %d" % (
+            wgs, per, rep, "each value once" if ok else "NOT a permutation", int(counter.item())))
+        assert ok
+        assert int(counter.item()) == wgs * per
+        # a workgroup's own claims increase
+        assert (np.diff(got.reshape(wgs, per), axis=1) > 0).all()

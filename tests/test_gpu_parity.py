@@ -157,11 +157,21 @@ def test_parity_full_size_mixed_sampled():
 def test_parity_full_size_long_decode():
     """Long-context decode at full size (8 requests, contexts 32K..128K): every
     row against the oracle (up to 121 splits per row: the long merge folds
-    them in chunks of 64)."""
+    them in chunks of 64).  The batch has more split items than the split
+    launch has workgroups, so the later items go to whichever workgroups ask
+    first: a second run (another assignment) and the first and last requests
+    alone (a few hundred items, no claims) give the same bits."""
     call = W.config4()
     U.say("full cfg4: kv=%.2f GB max_n=%d" % (call.kv_bytes() / 1e9, call.max_context_len))
     out = U.gpu_run(call, poison=False)
     U.say("  %s" % U.parity(call, out))
+    rows = U.by_position(call, out)
+    again = U.gpu_run(call, poison=True)
+    n = U.assert_same_bits(rows, U.by_position(call, again), min_common=len(call.reqs))
+    for i in (0, len(call.reqs) - 1):
+        sub = call.subcall([i])
+        n += U.assert_same_bits(rows, U.by_position(sub, U.gpu_run(sub)))
+    U.say("  %d rows bit-identical across runs and alone" % n)
 
 
 def test_parity_full_size_verify_sampled():
