@@ -2,7 +2,9 @@
 cannot allocate device memory): through the C ABI, its output equals
 vd_attn_forward's with a caller workspace bit for bit, on consecutive calls
 that reuse the library's static scratch, each later call smaller than the one
-before -- a full-size 8B decode batch, then a mixed batch whose new tokens
+before -- a long-context decode batch with more split items than the split
+launch has workgroups (the later items claimed from a counter kept in the
+scratch), a full-size 8B decode batch, then a mixed batch whose new tokens
 are written by the plan launch, then a prefix-shared verify batch (the
 shared-prefix pass) -- and the rows are within tolerance of the oracle."""
 from __future__ import annotations
@@ -52,6 +54,9 @@ def run_both(call, append=False):
 
 def test_noalloc_equals_forward_on_consecutive_calls():
     calls = [
+        # 6 requests x 8 KV heads x 88-108 splits: about 4,700 split items
+        ("long-context decode, head dim 64", W.config4(batch=6, lo=90000, hi=110000,
+                                                        shape=W.Shape(16, 8, 64)), False),
         ("8B decode, 64 requests", W.config2(), False),
         ("mixed, new tokens handed over", W.config3(num_prefill=2, chunk=96, max_off=900,
                                                     num_decode=10, dec_lo=60, dec_hi=1500), True),
