@@ -1107,8 +1107,9 @@ __device__ __forceinline__ void split_item(const Params& P, int r, int g, int k,
 // to 1, requests ascending) -- and each die (XCD: workgroup id mod the
 // die count, 8 on a whole MI355X) takes a contiguous range of the list: with
 // 8 KV heads and 8 dies XCD x runs head x, so a page read by several requests
-// stays in one L2, and within an XCD the shortest
-// items start last.
+// stays in one L2, and within an XCD the shortest items start last.  (When a
+// launch claims its later slots from a counter, only each workgroup's first
+// item comes from its die's range; the claimed slots interleave the dies.)
 constexpr int kInWaveChunks = 4;
 constexpr int kInWaveMaxSeqs = 64 * kInWaveChunks;
 // At most this many requests on the chunk path are put in longest-first
@@ -2563,7 +2564,8 @@ int run_splits(const Params& P0, bool stream_kv, hipStream_t s, hipEvent_t e0 = 
   Params P = P0;
   // upper bound of the split items (the work-list length); a workgroup stops
   // at its first slot past the call's items.  Workgroups that plan for
-  // themselves take XCD-contiguous ranges of the items.
+  // themselves take XCD-contiguous ranges of the items (their first items
+  // only, when the later ones are claimed).
   const int64_t items = split_slots(P);
   if (items > INT32_MAX - 8) return VD_ERR_INVALID_ARG;
   // at most about twice the wavefronts the chip holds at once (4 SIMDs per
