@@ -1136,7 +1136,8 @@ __device__ __forceinline__ int wave_scan_dpp(int v) {
   return v;
 }
 
-__device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, SplitRef& out) {
+__device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, SplitRef& out,
+                                                  int* hist) {
   constexpr int C = kInWaveChunks;
   const int lane = __lane_id();
   const unsigned long long below = (1ull << lane) - 1;
@@ -1214,16 +1215,23 @@ __device__ __forceinline__ bool inwave_split_item(const Params& P, int vb, Split
     }
   } else {
     idx -= whole;
-    // the tile counts some request's last split has (bit t), longest first
-    int bits = 0;
+    // Items of each tile count t (1 .. 16) of the last partial splits, in an
+    // LDS histogram (the workgroup is this one wavefront); then lane l holds
+    // the items of the classes 16 .. 16 - l (longest first), and the first lane
+    // whose count passes idx names the item's class.
+    if (lane <= kTilesPerSplit) hist[lane] = 0;
+    __syncthreads();
 #pragma unroll
-    for (int c = 0; c < C; ++c) bits |= cls[c] > 0 ? 1 << cls[c] : 0;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) bits |= __shfl_xor(bits, o, 64);
-    unsigned present = uni(bits);
-    while (present && j < 0) {
-      const int t = 31 - __builtin_clz(present);
-      present &= ~(1u << t);
+    for (int c = 0; c < C; ++c)
+      if (cls[c] > 0) atomicAdd(&hist[cls[c]], hv[c]);
+    __syncthreads();
+    const int ht = lane < kTilesPerSplit ? hist[kTilesPerSplit - lane] : 0;
+    const int upto = wave_scan_dpp(ht);
+    const unsigned long long past = __ballot(upto > idx);
+    if (past != 0) {
+      const int l = __builtin_ctzll(past);
+      const int t = kTilesPerSplit - l;
+      idx -= __builtin_amdgcn_readlane(upto - ht, l);  // items of the longer classes
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         const unsigned long long m = __ballot(cls[c] == t);
@@ -1510,6 +1518,7 @@ __device__ __forceinline__ bool append_unit(const Params& P, int u, uint16_t* ld
 template <int D, bool WIN, bool NT, int NA>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(NA == 1 || D == 64 ? 2 : 1))) void split_kernel(Params P) {
   __shared__ __attribute__((aligned(16))) uint16_t vlds[kMaxNewRows * D];
+  __shared__ int hist[kTilesPerSplit + 1];  // the planner's items per last-split tile count
   // The last append_wgs workgroups write the new tokens of the chunk-path
   // requests (units b - grid, b - grid + append_wgs, ...): dispatched after
   // every split workgroup, they run in the launch's tail, when the shortest
@@ -1538,7 +1547,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(NA == 1 || D
     Req R;
     if (P.inwave) {
       SplitRef it;
-      const bool found = inwave_split_item(P, vb, it);
+      const bool found = inwave_split_item(P, vb, it, hist);
       per_xcd = it.per_xcd;
       claims = claims && (per_xcd << P.xcd_shift) > grid;
       if (!found) {
