@@ -174,6 +174,32 @@ def test_parity_full_size_long_decode():
     U.say("  %d rows bit-identical across runs and alone" % n)
 
 
+def test_claimed_items_with_empty_slots_in_the_last_die_range():
+    """3 KV heads: 4,461 split items, not a multiple of the 8 dies, so the
+    last die's range ends with 3 slots that hold no item; a workgroup that
+    claims one of them claims again.  Sampled rows against the oracle, a
+    second run and requests alone bit for bit."""
+    rng = W.rng_for(8, 0)
+    sh = W.Shape(12, 3, 128)
+    prompts, reqs = [], []
+    for r in range(13):
+        n = int(rng.integers(110000, 125001))
+        prompts.append(W.make_prompt(sh, n, 8, r, q_window=1))
+        reqs.append(W.Req(r, n, 1))
+    call = W.place(sh, prompts, reqs, rng)
+    items = sum((r.n - 1) // 1024 + 1 for r in reqs) * sh.num_kv_heads
+    assert items > 4096 and items % 8 != 0, items
+    U.say("3 KV heads: %d requests, %d split items" % (len(reqs), items))
+    out = U.gpu_run(call)
+    U.say("  %s" % U.parity(call, out, rows=[0, 6, 12]))
+    rows = U.by_position(call, out)
+    n = U.assert_same_bits(rows, U.by_position(call, U.gpu_run(call)), min_common=len(reqs))
+    for i in (0, 12):
+        sub = call.subcall([i])
+        n += U.assert_same_bits(rows, U.by_position(sub, U.gpu_run(sub)))
+    U.say("  %d rows bit-identical across runs and alone" % n)
+
+
 def test_parity_full_size_verify_sampled():
     """70B prefix-shared verify at full size (256 requests on a shared
     2048-token prefix, s = 4 / 1)."""
